@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Throughput of the per-batch matching step on one MI355X.
+
+A step is one pass of the whole path over one batch: nearest cached prompts
+(cosine top-k over every cache entry), optimal level and capacity-constrained
+placement, and the gather of the cached latents.  Inputs are seeded synthetic
+embeddings already resident in HBM.  Caches that fit in the 256 MB Infinity
+Cache are rotated over several copies so every step reads its cache from HBM.
+
+Prints one JSON line: prompts matched per second (whole step), plus the
+similarity kernel's own time from HIP events recorded around it, its roofline
+fraction, and the float64 CPU reference timed on a bounded sample.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prompts matched/sec and cache-entry×query sims/sec; % HBM or MFMA peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0, "e4m3": 5000.0}
+MALL_BYTES = 256 << 20
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """Raw hipEvent_t pairs through the HIP runtime (the library records them on its stream)."""
+
+    def __init__(self, n):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.pairs = []
+        for _ in range(n):
+            a, b = ctypes.c_void_p(), ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(a)) == 0
+            assert self.hip.hipEventCreate(ctypes.byref(b)) == 0
+            self.pairs.append((a, b))
+
+    def elapsed_ms(self, i):
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), self.pairs[i][0], self.pairs[i][1])
+        assert rc == 0, f"hipEventElapsedTime failed ({rc})"
+        return ms.value
+
+    def close(self):
+        for a, b in self.pairs:
+            self.hip.hipEventDestroy(a)
+            self.hip.hipEventDestroy(b)
+
+
+def alg_bytes(w):
+    """Bytes the match step must move: the cache once, its row factors, the
+    queries and scales, and the top-k output."""
+    eb = {"f32": 4, "f16": 2, "bf16": 2, "e4m3": 1}[w.dtype]
+    scale = 4 if w.dtype == "e4m3" else 0
+    return w.N * w.d * eb + 4 * w.N + w.B * (w.d * eb + scale) + 8 * w.B * w.k
+
+
+def cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta, n_queries):
+    """The float64 reference on the first n_queries queries against the full cache."""
+    import numpy as np
+    from oracle import oracle
+    from paper_2502_06798_amd.synth import host_view
+    eh, qh = host_view(e), host_view(q[:n_queries])
+    esh, qsh = host_view(es), host_view(None if qs is None else qs[:n_queries])
+    e_sq, _, _ = oracle.row_sqnorms(w.dtype, eh, esh)
+    t0 = time.perf_counter()
+    q_sq, _, _ = oracle.row_sqnorms(w.dtype, qh, qsh)
+    ts, ti = oracle.topk(w.dtype, qh, qsh, eh, esh, w.k, q_sq=q_sq, e_sq=e_sq)
+    lv = oracle.levels(ts[:, 0], theta)
+    oracle.assign(lv, w.L, lvl, cap, queue)
+    dt = time.perf_counter() - t0
+    return {"value": round(n_queries / dt, 3), "unit": "prompts/s", "cores": oracle.max_threads(),
+            "kind": "oracle",
+            "sample": f"{n_queries} of {w.B} queries of {w.name} against all {w.N} entries "
+                      f"(top-{w.k}, levels, assignment), {dt:.2f} s; the entry norms are "
+                      "computed once outside the timed part"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="b256_n100k_d768_f16")
+    ap.add_argument("--copies", type=int, default=0, help="cache copies rotated per step (0 = auto)")
+    ap.add_argument("--cpu-queries", type=int, default=256)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU row-sharded design is described but not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2502_06798_amd as apc
+    from paper_2502_06798_amd import synth
+
+    apc.load()
+    torch.cuda.set_device(0)
+    w = synth.BY_NAME[args.workload]
+    log(f"generating {w.name}")
+    C = synth.centres(w, "cuda")
+    e, es = synth.entries(w, "cuda", C)
+    q, qs = synth.queries(w, "cuda", C)
+    del C
+    pool = synth.latents(w, "cuda")
+    soe = synth.slot_map(w, "cuda")
+    lvl, cap, queue = synth.instances(w)
+    theta, K = synth.thresholds(w)
+
+    cache_bytes = e.numel() * e.element_size()
+    copies = args.copies or (1 if cache_bytes > MALL_BYTES else min(8, -(-(5 * MALL_BYTES) // cache_bytes)))
+    embs = [e] + [e.clone() for _ in range(copies - 1)]
+    caches = [apc.apc_build_cache(x, es, pool, soe) for x in embs]
+    step = apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes)
+    torch.cuda.synchronize()
+
+    def run(i):
+        step.cache = caches[i % copies]
+        step.run(q, qs)
+
+    log(f"warmup {args.warmup} steps, {copies} cache copies")
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+
+    ev = HipEvents(args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        apc.apc_set_kernel_events(ev.pairs[i][0], ev.pairs[i][1])
+        run(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kern_ms = float(np.mean([ev.elapsed_ms(i) for i in range(args.steps)]))
+    ev.close()
+    wall = t1 - t0
+    ms_per_step = wall / args.steps * 1e3
+
+    flops = 2.0 * w.B * w.N * w.d
+    nbytes = alg_bytes(w)
+    ai = flops / nbytes
+    ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if ai < ridge:
+        achieved = nbytes / (kern_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_TFLOPS[w.dtype],
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[w.dtype], 4), "traffic": None}
+
+    out = {
+        "metric": METRIC,
+        "value": round(w.B * args.steps / wall, 1),
+        "unit": "prompts/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded clustered Gaussian embeddings standing in for prompt embeddings)",
+        "config": {"workload": w.name, "B": w.B, "N": w.N, "d": w.d, "k": w.k, "levels": w.L,
+                   "instances": w.n_inst, "capacity": w.cap, "latent_bytes": w.latent_bytes,
+                   "cache_copies": copies},
+        "sims_per_s": round(w.B * w.N / (kern_ms * 1e-3), 1),
+        "sim_kernel_ms": round(kern_ms, 5),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU reference")
+        out["cpu_baseline"] = cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta,
+                                           min(args.cpu_queries, w.B))
+    for c in caches:
+        c.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,185 @@
+/*
+ * apc — approximate-cache prompt matching on MI355X (gfx950).
+ *
+ * C ABI of the per-batch step of prompt-aware scheduling for diffusion
+ * serving with approximate caching (Approach section of the paper): for a
+ * batch of prompt embeddings, find the nearest cached prompts, turn the best
+ * closeness into an optimal skip level K, place every prompt on a model
+ * instance under per-instance capacity (redirecting to other levels when the
+ * optimal one is full), and gather the cached intermediate state (latent)
+ * each placed prompt will start denoising from.
+ *
+ * Conventions shared by every call:
+ *  - Pointers are DEVICE pointers unless marked (host).  All device buffers
+ *    belong to the caller and must be 16-byte aligned.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Calls enqueue work on it and return without waiting, except
+ *    apc_build_cache, which waits once to report data errors.
+ *  - Arguments are checked on the host before anything is enqueued; on a
+ *    non-OK status nothing was enqueued and no output was written, except
+ *    APC_E_HIP (a launch failed; outputs are unspecified).
+ *  - apc_last_error() gives a thread-local message for the last failing call.
+ *  - Calls on different streams may run concurrently when they write
+ *    disjoint buffers (each match call needs its own workspace).
+ */
+#ifndef APC_H
+#define APC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* storage type of embeddings and queries */
+typedef enum {
+    APC_F32 = 0,   /* IEEE binary32 */
+    APC_F16 = 1,   /* IEEE binary16 */
+    APC_BF16 = 2,  /* bfloat16 */
+    APC_E4M3 = 3   /* OCP e4m3fn codes with one float32 scale per row */
+} apc_dtype;
+
+typedef enum {
+    APC_OK = 0,
+    APC_E_ARG = 1,        /* bad size, pointer, alignment or count */
+    APC_E_DTYPE = 2,      /* unknown storage type */
+    APC_E_TABLE = 3,      /* bad threshold or instance table */
+    APC_E_NONFINITE = 4,  /* a cache row holds Inf/NaN, or a row scale is not finite and > 0 */
+    APC_E_ZERO_NORM = 5,  /* a cache row has zero norm */
+    APC_E_WORKSPACE = 6,  /* workspace smaller than apc_match_workspace() asks */
+    APC_E_NOMEM = 7,      /* device or host allocation failed */
+    APC_E_HIP = 8         /* a HIP runtime call or kernel launch failed */
+} apc_status;
+
+#define APC_MAX_K 64          /* largest neighbour count per query */
+#define APC_MAX_LEVELS 32     /* largest number of skip levels L */
+#define APC_MAX_INST 256      /* largest number of model instances */
+
+/* opaque, immutable after build */
+typedef struct apc_cache apc_cache;
+
+/*
+ * Build a handle over a cache of n prompt embeddings (the approximate cache
+ * of the Introduction: prior prompts whose intermediate states can be
+ * reused).
+ *
+ * emb           n x d row-major elements of type dt; d * element size must be
+ *               a multiple of 16 bytes.
+ * row_scale     n float32 (APC_E4M3 only, else NULL): element value = code *
+ *               scale.  Scales must be finite and > 0.  The cosine does not
+ *               depend on them.
+ * latents       n_slots x latent_bytes cached latents, or NULL with n_slots = 0
+ *               (no gather).  latent_bytes must be a multiple of 16.
+ * slot_of_entry n int32: the latent slot of each entry, -1 = not resident;
+ *               NULL = entry i lives in slot i (then n_slots >= n).
+ *
+ * The handle BORROWS emb, row_scale, latents and slot_of_entry: they must
+ * stay alive and unchanged until apc_destroy_cache.  The library owns only
+ * n float32 row factors (1 / norm) on the current device.  Waits for the
+ * stream once and returns APC_E_NONFINITE / APC_E_ZERO_NORM / APC_E_ARG
+ * (slot out of range) for bad data, with *out left NULL.
+ */
+apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb,
+                           const float* row_scale, const void* latents, int64_t n_slots,
+                           int64_t latent_bytes, const int32_t* slot_of_entry, void* stream,
+                           apc_cache** out /* host */);
+
+/* Frees the handle and its row factors (NULL is a no-op).  The caller must
+   make sure no call using the handle is still running. */
+void apc_destroy_cache(apc_cache* c);
+
+/*
+ * Row factors f = 1 / |x| of n rows of type dt (for APC_E4M3 the norm of
+ * the codes; the scale cancels in the cosine), written to out (n float32).
+ * Rows with a non-finite element or zero norm get NaN.  This is the
+ * per-row preparation of both the cache build and the query batch.
+ */
+apc_status apc_row_factors(apc_dtype dt, int64_t n, int32_t d, const void* rows, float* out,
+                           void* stream);
+
+/* Copies the handle's n entry factors to out (n float32, device). */
+apc_status apc_cache_row_factors(const apc_cache* c, float* out, void* stream);
+
+/* Workspace bytes apc_match_batch needs for b queries and k neighbours. */
+apc_status apc_match_workspace(const apc_cache* c, int32_t b, int32_t k, size_t* bytes /* host */);
+
+/*
+ * Nearest cached prompts (Query Dispatcher, "retrieves the nearest cache"):
+ * for each of the b query rows, the k cache entries with the highest cosine
+ * similarity of the stored vectors,
+ *     s(q, e) = clamp(<q, e> * f_q * f_e, -1, 1),   f = 1 / |row|,
+ * accumulated in float32 over all d elements (no split over d, so scores are
+ * deterministic), in the order (score desc, entry index asc).
+ *
+ * q          b x d row-major queries in the cache's type.
+ * q_scale    b float32 (APC_E4M3 only, else NULL).
+ * top_score  b x k float32, top_idx b x k int32 (row q at q * k).
+ * ws         workspace of at least apc_match_workspace() bytes.
+ * 1 <= k <= min(n, APC_MAX_K).  b = 0 is a no-op.
+ * A query row that is non-finite, has zero norm or (APC_E4M3) a scale that
+ * is not finite and > 0 gets top_score = NaN and top_idx = -1.
+ */
+apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_scale, int32_t b,
+                           int32_t k, float* top_score, int32_t* top_idx, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/*
+ * Optimal level and capacity-constrained placement (Approach: optimal-K,
+ * redirection to K' < K or to the closest K' > K with Eq. 1 charging
+ * degradation only upwards; greedy route-and-batch filling the longest
+ * queue first).
+ *
+ * top_score   b rows of stride ld (>= 1) float32; column 0 is the best score.
+ * theta, K    (host) L float32 thresholds and L skip counts, both strictly
+ *             increasing, thresholds finite, K > 0; 0 <= L <= APC_MAX_LEVELS.
+ *             Level lam = #{l : best >= theta[l]} (0 = no skip, K = 0).
+ * inst_level, inst_cap, inst_queue (host) n_inst <= APC_MAX_INST instances:
+ *             level in 0..L, capacity >= 0 (total <= INT32_MAX), queue
+ *             length (NULL = all 0).
+ * Outputs (device): opt_level[b] = lam; out_level/out_inst/out_slot[b] = the
+ *             placement (-1 when no capacity is left anywhere); inst_fill[n_inst]
+ *             = queries placed per instance.
+ * Placement: rounds r = 0..L over the preference list
+ *             [lam, lam-1, .., 0, lam+1, .., L]; in each round unassigned
+ *             queries, in index order, take a place at their r-th preference
+ *             while it has capacity.  Within a level, places are handed out
+ *             over its instances ordered by (queue desc, index asc), each up
+ *             to its capacity, slots from 0.
+ */
+apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L,
+                      const float* theta /* host */, const int32_t* K /* host */, int32_t n_inst,
+                      const int32_t* inst_level /* host */, const int32_t* inst_cap /* host */,
+                      const int32_t* inst_queue /* host, nullable */, int32_t* opt_level,
+                      int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
+                      int32_t* inst_fill, void* stream);
+
+/*
+ * Latent gather (the cached intermediate state a placed prompt starts from):
+ * for each query with out_level > 0 whose top-1 entry top_idx[q * ld] has a
+ * resident latent, copy it to batch_latents[(out_inst * slots_per_inst +
+ * out_slot) * latent_bytes] and set hit[q] = 1; otherwise hit[q] = 0 and that
+ * batch slot is not written.  out_slot must be < slots_per_inst for every
+ * copied query (as apc_assign produces with slots_per_inst >= max capacity).
+ */
+apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
+                              const int32_t* out_level, const int32_t* out_inst,
+                              const int32_t* out_slot, int32_t n_inst, int32_t slots_per_inst,
+                              void* batch_latents, int32_t* hit, void* stream);
+
+/*
+ * Measurement hook (for benchmarks and profilers, not for the method):
+ * the next apc_match_batch call on this thread records `start` (a
+ * hipEvent_t) on its stream right before the similarity/top-k kernel and
+ * `stop` right after it, then forgets both.  NULL, NULL clears the hook.
+ */
+apc_status apc_set_kernel_events(void* start, void* stop);
+
+const char* apc_status_str(apc_status s);
+const char* apc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APC_H */

@@ -127,29 +127,30 @@ int oracle_decode(int dt, const void* rows, const float* scale, int64_t n, int32
     return OR_OK;
 }
 
-/* Squared Euclidean norm of each row (sequential sum of squares).
- * Returns the first bad row's status: non-finite element or zero norm. */
+/* Squared Euclidean norm of each row (sequential sum of squares; rows run in
+ * parallel).  Returns the first bad row's status: a non-finite element makes
+ * the sum non-finite (OR_E_NONFINITE); an all-zero row gives 0 (OR_E_ZERO_NORM). */
 int oracle_row_sqnorms(int dt, const void* rows, const float* scale, int64_t n, int32_t d,
                        double* sq, int64_t* bad_row)
 {
     if (!elem_bytes(dt) || n < 0 || d < 1 || (dt == OR_E4M3 && !scale) || !lut_ready) return OR_E_ARG;
-    *bad_row = -1;
-    int status = OR_OK;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(static)
+#endif
     for (int64_t r = 0; r < n; ++r) {
         double ss = 0.0;
-        int finite = 1;
         for (int32_t i = 0; i < d; ++i) {
             double x = elem(dt, rows, scale, r, d, i);
-            if (!isfinite(x)) finite = 0;
             ss += x * x;
         }
         sq[r] = ss;
-        if (status == OR_OK && (!finite || !(ss > 0.0) || !isfinite(ss))) {
-            status = finite && isfinite(ss) ? OR_E_ZERO_NORM : OR_E_NONFINITE;
-            *bad_row = r;
-        }
     }
-    return status;
+    *bad_row = -1;
+    for (int64_t r = 0; r < n; ++r) {
+        if (!isfinite(sq[r])) { *bad_row = r; return OR_E_NONFINITE; }
+        if (!(sq[r] > 0.0)) { *bad_row = r; return OR_E_ZERO_NORM; }
+    }
+    return OR_OK;
 }
 
 /* cosine of a decoded query row qv (squared norm sq_q) and stored entry row ei

@@ -1,0 +1,336 @@
+// C ABI of the matching library: argument checks, handle lifetime,
+// workspace sizing and kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <climits>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "apc_internal.h"
+
+struct apc_cache {
+    apc_dtype dt;
+    int64_t n;
+    int32_t d;
+    const void* emb;
+    const float* row_scale;
+    const void* latents;
+    int64_t n_slots;
+    int64_t latent_bytes;
+    const int32_t* slot_of_entry;
+    float* fe;          // owned: n row factors, padded with zeros to a multiple of 256
+    int device;
+};
+
+namespace {
+
+thread_local std::string g_err;
+thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+apc_status fail(apc_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+apc_status fail(apc_status s, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+apc_status ok()
+{
+    g_err.clear();
+    return APC_OK;
+}
+
+apc_status hip_fail(hipError_t e, const char* what)
+{
+    return fail(APC_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_dtype(int dt) { return dt >= APC_F32 && dt <= APC_E4M3; }
+
+apc_status check_rows(apc_dtype dt, int64_t n, int32_t d, const void* rows, const char* what)
+{
+    if (!valid_dtype(dt)) return fail(APC_E_DTYPE, "unknown dtype %d", (int)dt);
+    if (n < 0 || d < 1) return fail(APC_E_ARG, "%s: need n >= 0 and d >= 1 (n=%lld d=%d)", what, (long long)n, d);
+    if (((int64_t)d * apc::elem_bytes(dt)) % 16 != 0)
+        return fail(APC_E_ARG, "%s: row of %d elements is not a multiple of 16 bytes", what, d);
+    if (n > 0 && (!rows || !aligned16(rows)))
+        return fail(APC_E_ARG, "%s: rows must be a non-NULL 16-byte aligned device pointer", what);
+    return APC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* apc_status_str(apc_status s)
+{
+    switch (s) {
+    case APC_OK: return "ok";
+    case APC_E_ARG: return "invalid argument";
+    case APC_E_DTYPE: return "unknown dtype";
+    case APC_E_TABLE: return "invalid threshold or instance table";
+    case APC_E_NONFINITE: return "non-finite value";
+    case APC_E_ZERO_NORM: return "zero-norm row";
+    case APC_E_WORKSPACE: return "workspace too small";
+    case APC_E_NOMEM: return "out of memory";
+    case APC_E_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char* apc_last_error(void) { return g_err.c_str(); }
+
+apc_status apc_set_kernel_events(void* start, void* stop)
+{
+    if ((start == nullptr) != (stop == nullptr))
+        return fail(APC_E_ARG, "apc_set_kernel_events: give both events or neither");
+    g_ev_start = static_cast<hipEvent_t>(start);
+    g_ev_stop = static_cast<hipEvent_t>(stop);
+    return ok();
+}
+
+apc_status apc_row_factors(apc_dtype dt, int64_t n, int32_t d, const void* rows, float* out, void* stream)
+{
+    apc_status st = check_rows(dt, n, d, rows, "apc_row_factors");
+    if (st != APC_OK) return st;
+    if (n > 0 && !out) return fail(APC_E_ARG, "apc_row_factors: out is NULL");
+    if (n == 0) return ok();
+    hipError_t e = apc::launch_row_factors(dt, n, d, rows, nullptr, nullptr, 0, out, nullptr,
+                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "row factor launch");
+    return ok();
+}
+
+apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, const float* row_scale,
+                           const void* latents, int64_t n_slots, int64_t latent_bytes,
+                           const int32_t* slot_of_entry, void* stream, apc_cache** out)
+{
+    if (!out) return fail(APC_E_ARG, "apc_build_cache: out is NULL");
+    *out = nullptr;
+    apc_status st = check_rows(dt, n, d, emb, "apc_build_cache");
+    if (st != APC_OK) return st;
+    if (n < 1 || n >= INT32_MAX)
+        return fail(APC_E_ARG, "apc_build_cache: need 1 <= n < 2^31 - 1 entries (n=%lld)", (long long)n);
+    if ((dt == APC_E4M3) != (row_scale != nullptr))
+        return fail(APC_E_ARG, "apc_build_cache: row_scale is required for e4m3 and only for e4m3");
+    if (n_slots < 0 || latent_bytes < 0)
+        return fail(APC_E_ARG, "apc_build_cache: negative n_slots or latent_bytes");
+    if (n_slots > 0) {
+        if (!latents || !aligned16(latents))
+            return fail(APC_E_ARG, "apc_build_cache: latents must be a 16-byte aligned device pointer");
+        if (latent_bytes <= 0 || latent_bytes % 16 != 0)
+            return fail(APC_E_ARG, "apc_build_cache: latent_bytes must be a positive multiple of 16");
+        if (!slot_of_entry && n_slots < n)
+            return fail(APC_E_ARG, "apc_build_cache: identity slot map needs n_slots >= n");
+    } else if (latents || slot_of_entry) {
+        return fail(APC_E_ARG, "apc_build_cache: latents/slot_of_entry given with n_slots = 0");
+    }
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+
+    apc_cache* c = new (std::nothrow) apc_cache{};
+    if (!c) return fail(APC_E_NOMEM, "apc_build_cache: host allocation failed");
+    const int64_t n_pad = (n + 255) / 256 * 256;
+    apc::BuildStatus* dst = nullptr;
+    apc::BuildStatus hst{};
+    if ((e = hipMalloc(&c->fe, sizeof(float) * n_pad)) != hipSuccess) {
+        delete c;
+        return fail(APC_E_NOMEM, "apc_build_cache: hipMalloc of %lld row factors: %s", (long long)n,
+                    hipGetErrorString(e));
+    }
+    auto cleanup = [&]() {
+        if (dst) (void)hipFree(dst);
+        (void)hipFree(c->fe);
+        delete c;
+    };
+    if ((e = hipMalloc(&dst, sizeof(apc::BuildStatus))) != hipSuccess) {
+        cleanup();
+        return fail(APC_E_NOMEM, "apc_build_cache: hipMalloc: %s", hipGetErrorString(e));
+    }
+    hst.first_bad = ~0ull;
+    if ((e = hipMemsetAsync(c->fe + n, 0, sizeof(float) * (n_pad - n), s)) != hipSuccess ||
+        (e = hipMemcpyAsync(dst, &hst, sizeof hst, hipMemcpyHostToDevice, s)) != hipSuccess ||
+        (e = apc::launch_row_factors(dt, n, d, emb, row_scale, slot_of_entry, n_slots, c->fe, dst, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(&hst, dst, sizeof hst, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess) {
+        cleanup();
+        return hip_fail(e, "apc_build_cache");
+    }
+    if (hst.flags) {
+        const unsigned long long r = hst.first_bad;
+        cleanup();
+        if (hst.flags & apc::ST_NONFINITE)
+            return fail(APC_E_NONFINITE, "apc_build_cache: non-finite values (first bad row %llu)", r);
+        if (hst.flags & apc::ST_SCALE)
+            return fail(APC_E_NONFINITE, "apc_build_cache: row scale not finite and > 0 (first bad row %llu)", r);
+        if (hst.flags & apc::ST_ZERO)
+            return fail(APC_E_ZERO_NORM, "apc_build_cache: zero-norm row (first bad row %llu)", r);
+        return fail(APC_E_ARG, "apc_build_cache: slot_of_entry out of range (first bad entry %llu)", r);
+    }
+    (void)hipFree(dst);
+    c->dt = dt;
+    c->n = n;
+    c->d = d;
+    c->emb = emb;
+    c->row_scale = row_scale;
+    c->latents = latents;
+    c->n_slots = n_slots;
+    c->latent_bytes = latent_bytes;
+    c->slot_of_entry = slot_of_entry;
+    c->device = dev;
+    *out = c;
+    return ok();
+}
+
+void apc_destroy_cache(apc_cache* c)
+{
+    if (!c) return;
+    (void)hipFree(c->fe);
+    delete c;
+}
+
+apc_status apc_cache_row_factors(const apc_cache* c, float* out, void* stream)
+{
+    if (!c || !out) return fail(APC_E_ARG, "apc_cache_row_factors: NULL argument");
+    hipError_t e = hipMemcpyAsync(out, c->fe, sizeof(float) * c->n, hipMemcpyDeviceToDevice,
+                                  static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_cache_row_factors");
+    return ok();
+}
+
+apc_status apc_match_workspace(const apc_cache* c, int32_t b, int32_t k, size_t* bytes)
+{
+    if (!c || !bytes) return fail(APC_E_ARG, "apc_match_workspace: NULL argument");
+    if (b < 0) return fail(APC_E_ARG, "apc_match_workspace: b < 0");
+    if (k < 1 || k > APC_MAX_K || k > c->n)
+        return fail(APC_E_ARG, "apc_match_workspace: need 1 <= k <= min(n, %d) (k=%d)", APC_MAX_K, k);
+    *bytes = b == 0 ? 0 : apc::plan_match(c->dt, c->n, c->d, b, k).bytes;
+    return ok();
+}
+
+apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_scale, int32_t b, int32_t k,
+                           float* top_score, int32_t* top_idx, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!c) return fail(APC_E_ARG, "apc_match_batch: NULL cache");
+    if (b < 0) return fail(APC_E_ARG, "apc_match_batch: b < 0");
+    if (k < 1 || k > APC_MAX_K || k > c->n)
+        return fail(APC_E_ARG, "apc_match_batch: need 1 <= k <= min(n, %d) (k=%d)", APC_MAX_K, k);
+    if (b == 0) return ok();
+    apc_status st = check_rows(c->dt, b, c->d, q, "apc_match_batch queries");
+    if (st != APC_OK) return st;
+    if ((c->dt == APC_E4M3) != (q_scale != nullptr))
+        return fail(APC_E_ARG, "apc_match_batch: q_scale is required for e4m3 and only for e4m3");
+    if (!top_score || !top_idx || !aligned16(top_score) || !aligned16(top_idx))
+        return fail(APC_E_ARG, "apc_match_batch: outputs must be 16-byte aligned device pointers");
+    const apc::MatchPlan p = apc::plan_match(c->dt, c->n, c->d, b, k);
+    if (!ws || ws_bytes < p.bytes || (reinterpret_cast<uintptr_t>(ws) & 255u))
+        return fail(APC_E_WORKSPACE, "apc_match_batch: workspace needs %zu bytes, 256-byte aligned (got %zu)",
+                    p.bytes, ws_bytes);
+    hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
+    g_ev_start = g_ev_stop = nullptr;
+    hipError_t e = apc::launch_match(p, c->dt, c->n, c->d, c->emb, c->fe, q, q_scale, b, k, top_score,
+                                     top_idx, ws, static_cast<hipStream_t>(stream), ev0, ev1);
+    if (e != hipSuccess) return hip_fail(e, "apc_match_batch launch");
+    return ok();
+}
+
+apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
+                      const int32_t* K, int32_t n_inst, const int32_t* inst_level, const int32_t* inst_cap,
+                      const int32_t* inst_queue, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                      int32_t* out_slot, int32_t* inst_fill, void* stream)
+{
+    if (b < 0 || ld < 1) return fail(APC_E_ARG, "apc_assign: need b >= 0 and ld >= 1");
+    if (L < 0 || L > APC_MAX_LEVELS) return fail(APC_E_TABLE, "apc_assign: need 0 <= L <= %d", APC_MAX_LEVELS);
+    if (L > 0 && (!theta || !K)) return fail(APC_E_TABLE, "apc_assign: theta/K are NULL");
+    for (int l = 0; l < L; ++l) {
+        if (!std::isfinite(theta[l])) return fail(APC_E_TABLE, "apc_assign: theta[%d] is not finite", l);
+        if (K[l] <= 0) return fail(APC_E_TABLE, "apc_assign: K[%d] must be > 0", l);
+        if (l > 0 && !(theta[l] > theta[l - 1]))
+            return fail(APC_E_TABLE, "apc_assign: thresholds must be strictly increasing");
+        if (l > 0 && !(K[l] > K[l - 1])) return fail(APC_E_TABLE, "apc_assign: K must be strictly increasing");
+    }
+    if (n_inst < 0 || n_inst > APC_MAX_INST)
+        return fail(APC_E_TABLE, "apc_assign: need 0 <= n_inst <= %d", APC_MAX_INST);
+    if (n_inst > 0 && (!inst_level || !inst_cap)) return fail(APC_E_TABLE, "apc_assign: instance table is NULL");
+    int64_t total = 0;
+    for (int i = 0; i < n_inst; ++i) {
+        if (inst_level[i] < 0 || inst_level[i] > L)
+            return fail(APC_E_TABLE, "apc_assign: inst_level[%d] = %d not in 0..%d", i, inst_level[i], L);
+        if (inst_cap[i] < 0) return fail(APC_E_TABLE, "apc_assign: inst_cap[%d] < 0", i);
+        total += inst_cap[i];
+    }
+    if (total > INT32_MAX) return fail(APC_E_TABLE, "apc_assign: total capacity exceeds 2^31 - 1");
+    if (b > 0 && (!top_score || !opt_level || !out_level || !out_inst || !out_slot))
+        return fail(APC_E_ARG, "apc_assign: NULL device buffer");
+    if (n_inst > 0 && !inst_fill) return fail(APC_E_ARG, "apc_assign: inst_fill is NULL");
+
+    apc::AssignTable t{};
+    t.L = L;
+    t.n_inst = n_inst;
+    for (int l = 0; l < L; ++l) t.theta[l] = theta[l];
+    int order[APC_MAX_INST];
+    for (int i = 0; i < n_inst; ++i) order[i] = i;
+    std::stable_sort(order, order + n_inst, [&](int a, int c) {
+        const int qa = inst_queue ? inst_queue[a] : 0, qc = inst_queue ? inst_queue[c] : 0;
+        if (inst_level[a] != inst_level[c]) return inst_level[a] < inst_level[c];
+        if (qa != qc) return qa > qc;
+        return a < c;
+    });
+    int j = 0;
+    for (int p = 0; p <= L; ++p) {
+        t.level_first[p] = j;
+        int64_t cum = 0;
+        while (j < n_inst && inst_level[order[j]] == p) {
+            t.ord_inst[j] = (int16_t)order[j];
+            t.ord_cap[j] = inst_cap[order[j]];
+            t.ord_cum[j] = (int32_t)cum;
+            cum += inst_cap[order[j]];
+            ++j;
+        }
+        t.level_cap[p] = (int32_t)cum;
+    }
+    t.level_first[L + 1] = j;
+    if (b == 0 && n_inst == 0) return ok();
+    hipError_t e = apc::launch_assign(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot,
+                                      inst_fill, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_assign launch");
+    return ok();
+}
+
+apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
+                              const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                              int32_t n_inst, int32_t slots_per_inst, void* batch_latents, int32_t* hit,
+                              void* stream)
+{
+    if (!c) return fail(APC_E_ARG, "apc_gather_latents: NULL cache");
+    if (c->n_slots == 0) return fail(APC_E_ARG, "apc_gather_latents: the cache has no latents");
+    if (b < 0 || ld < 1 || n_inst < 0 || slots_per_inst < 0)
+        return fail(APC_E_ARG, "apc_gather_latents: need b >= 0, ld >= 1, n_inst >= 0, slots_per_inst >= 0");
+    if (b == 0) return ok();
+    if (!top_idx || !out_level || !out_inst || !out_slot || !hit)
+        return fail(APC_E_ARG, "apc_gather_latents: NULL device buffer");
+    if ((int64_t)n_inst * slots_per_inst > 0 && (!batch_latents || !aligned16(batch_latents)))
+        return fail(APC_E_ARG, "apc_gather_latents: batch_latents must be 16-byte aligned");
+    hipError_t e = apc::launch_gather(c->latents, c->n, c->n_slots, c->latent_bytes, c->slot_of_entry,
+                                      top_idx, ld, b, out_level, out_inst, out_slot, n_inst, slots_per_inst,
+                                      batch_latents, hit, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_gather_latents launch");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+// Internal declarations shared by the host library and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/apc.h"
+
+namespace apc {
+
+inline int elem_bytes(int dt)
+{
+    switch (dt) {
+    case APC_F32: return 4;
+    case APC_F16: case APC_BF16: return 2;
+    case APC_E4M3: return 1;
+    default: return 0;
+    }
+}
+
+// ---- row factors (cache build and query preparation) ----------------------
+// bits of the build status word
+enum : uint32_t { ST_NONFINITE = 1u, ST_ZERO = 2u, ST_SCALE = 4u, ST_SLOT = 8u };
+struct BuildStatus {
+    uint32_t flags;
+    uint32_t pad;
+    unsigned long long first_bad;   // lowest bad row (or entry) index
+};
+
+// f[r] = 1/|row r| (NaN for bad rows); when st != nullptr also records bad
+// rows, non-positive or non-finite scales and out-of-range slots.
+hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, const float* scale,
+                              const int32_t* slot_of_entry, int64_t n_slots, float* f,
+                              BuildStatus* st, hipStream_t s);
+
+// ---- similarity + top-k ----------------------------------------------------
+struct MatchPlan {
+    int kernel;        // kernel variant id
+    int bq;            // queries per workgroup tile
+    int qtiles;        // ceil(b / bq)
+    int splits;        // workgroups along the entries per query tile
+    int64_t b_pad;     // qtiles * bq
+    size_t off_fq, off_ps, off_pi, bytes;   // workspace layout
+};
+MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k);
+
+// ev_start/ev_stop (may be null) are recorded around the similarity kernel.
+hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb,
+                        const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
+                        float* top_score, int32_t* top_idx, void* ws, hipStream_t s,
+                        hipEvent_t ev_start, hipEvent_t ev_stop);
+
+// ---- assignment ------------------------------------------------------------
+struct AssignTable {
+    int32_t L;
+    int32_t n_inst;
+    float theta[APC_MAX_LEVELS];
+    int32_t level_cap[APC_MAX_LEVELS + 1];       // places per level
+    int32_t level_first[APC_MAX_LEVELS + 2];     // first ordered instance of each level
+    int16_t ord_inst[APC_MAX_INST];              // instances by (level, queue desc, index asc)
+    int32_t ord_cum[APC_MAX_INST];               // places of earlier instances of the same level
+    int32_t ord_cap[APC_MAX_INST];
+};
+
+hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t ld, int32_t b,
+                         int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                         int32_t* out_slot, int32_t* inst_fill, hipStream_t s);
+
+// ---- gather ----------------------------------------------------------------
+hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,
+                         const int32_t* slot_of_entry, const int32_t* top_idx, int32_t ld, int32_t b,
+                         const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                         int32_t n_inst, int32_t slots_per_inst, void* batch, int32_t* hit,
+                         hipStream_t s);
+
+}  // namespace apc

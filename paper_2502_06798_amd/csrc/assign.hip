@@ -1,0 +1,114 @@
+// Optimal level and capacity-constrained placement of a batch of queries.
+//
+// One workgroup of 1024 threads.  The level of query q is the number of
+// thresholds at or below its best score.  Placement runs rounds r = 0..L:
+// every unassigned query applies to the r-th entry of its preference list
+// [lam, lam-1, .., 0, lam+1, .., L]; a level accepts applicants in query
+// order while it has places left.  Within a round, levels do not interact,
+// so each 1024-query chunk computes every applicant's rank among the
+// applicants of its level with one wave ballot per level (prefix counts in
+// lane order) plus per-wave totals summed in wave order; chunks run in
+// query order.  Ranks therefore never depend on atomic ordering, and the
+// result is deterministic.  A placement of rank t at level p lands on the
+// level's instances ordered by (queue desc, index asc), each filled up to
+// its capacity.
+#include "apc_internal.h"
+
+namespace apc {
+namespace {
+
+constexpr int NT = 1024;
+constexpr int NWAVE = NT / 64;
+
+__global__ __launch_bounds__(NT) void k_assign(const AssignTable t, const float* __restrict__ top_score,
+                                                int32_t ld, int32_t b, int32_t* __restrict__ opt_level,
+                                                int32_t* __restrict__ out_level,
+                                                int32_t* __restrict__ out_inst,
+                                                int32_t* __restrict__ out_slot,
+                                                int32_t* __restrict__ inst_fill)
+{
+    __shared__ int used[APC_MAX_LEVELS + 1];
+    __shared__ int wcnt[NWAVE][APC_MAX_LEVELS + 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = t.L;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+    for (int q = tid; q < b; q += NT) {
+        const float best = top_score[(int64_t)q * ld];
+        int lam = 0;
+        for (int l = 0; l < L; ++l) lam += best >= t.theta[l];
+        opt_level[q] = lam;
+        out_level[q] = -1;
+        out_slot[q] = -1;
+    }
+    if (tid <= L) used[tid] = 0;
+    __syncthreads();
+
+    for (int r = 0; r <= L; ++r) {
+        for (int base = 0; base < b; base += NT) {
+            const int q = base + tid;
+            int want = -1;
+            if (q < b && out_level[q] < 0) {
+                const int lam = opt_level[q];
+                want = r <= lam ? lam - r : r;
+            }
+            int pre = 0;
+            for (int p = 0; p <= L; ++p) {
+                const uint64_t m = __ballot(want == p);
+                if (want == p) pre = __popcll(m & lt_mask);
+                if (lane == 0) wcnt[wave][p] = __popcll(m);
+            }
+            __syncthreads();
+            if (want >= 0) {
+                int rank = used[want] + pre;
+                for (int w = 0; w < wave; ++w) rank += wcnt[w][want];
+                if (rank < t.level_cap[want]) {
+                    out_level[q] = want;
+                    out_slot[q] = rank;           // admission rank until the instance pass below
+                }
+            }
+            __syncthreads();
+            if (tid <= L) {
+                int tot = 0;
+                for (int w = 0; w < NWAVE; ++w) tot += wcnt[w][tid];
+                const int u = used[tid] + tot;
+                used[tid] = u < t.level_cap[tid] ? u : t.level_cap[tid];
+            }
+            __syncthreads();
+        }
+    }
+
+    for (int q = tid; q < b; q += NT) {
+        const int p = out_level[q];
+        int inst = -1, slot = -1;
+        if (p >= 0) {
+            const int rank = out_slot[q];
+            for (int j = t.level_first[p]; j < t.level_first[p + 1]; ++j)
+                if (rank < t.ord_cum[j] + t.ord_cap[j]) {
+                    inst = t.ord_inst[j];
+                    slot = rank - t.ord_cum[j];
+                    break;
+                }
+        }
+        out_inst[q] = inst;
+        out_slot[q] = slot;
+    }
+    for (int p = 0; p <= L; ++p)
+        for (int j = t.level_first[p] + tid; j < t.level_first[p + 1]; j += NT) {
+            int f = used[p] - t.ord_cum[j];
+            f = f < 0 ? 0 : (f > t.ord_cap[j] ? t.ord_cap[j] : f);
+            inst_fill[t.ord_inst[j]] = f;
+        }
+}
+
+}  // namespace
+
+hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t ld, int32_t b,
+                         int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                         int32_t* out_slot, int32_t* inst_fill, hipStream_t s)
+{
+    k_assign<<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    return hipGetLastError();
+}
+
+}  // namespace apc

@@ -245,3 +245,16 @@ def instances(w: Workload):
 def thresholds(w: Workload):
     """(theta float32[L], K int32[L]) as host numpy arrays."""
     return np.array(w.theta, dtype=np.float32), np.array(w.K, dtype=np.int32)
+
+
+def host_view(t: Optional[torch.Tensor]):
+    """Host numpy array of a tensor's stored elements (same bytes and element
+    size: bfloat16 as int16, e4m3fn as uint8), or None."""
+    if t is None:
+        return None
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy()
+    if t.dtype == torch.float8_e4m3fn:
+        return t.view(torch.uint8).numpy()
+    return t.numpy()

@@ -1,17 +1,11 @@
 """Helpers shared by the tests (no arithmetic of the method)."""
-import numpy as np
-import torch
+from paper_2502_06798_amd.synth import host_view
 
 
-def stored_np(t: torch.Tensor) -> np.ndarray:
+def stored_np(t):
     """Host numpy view of a tensor's stored elements (same bytes, same element size)."""
-    t = t.detach().cpu().contiguous()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy()
-    if t.dtype == torch.float8_e4m3fn:
-        return t.view(torch.uint8).numpy()
-    return t.numpy()
+    return host_view(t)
 
 
 def np_or_none(t):
-    return None if t is None else t.detach().cpu().numpy()
+    return host_view(t)

@@ -1,0 +1,112 @@
+"""GPU parity on the five synthetic workloads at full size, in the launch
+configuration the benchmark times.
+
+Workloads 1-2: every query is checked against the float64 reference.
+Workloads 3-5: a seeded sample of queries (the reference is brute force over
+all N entries per query).  For every workload the levels of all B queries
+are checked against the reference on the GPU's best scores, the assignment
+is bit-exact given the GPU's levels, and the gathered latents are
+byte-exact given the GPU's top-1 and assignment.
+"""
+import gc
+import time
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2502_06798_amd import synth
+from tests._util import np_or_none, stored_np
+from tests.gpu_check import TOL, check_levels, check_topk, say
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE = {1: None, 2: None, 3: 48, 4: 24, 5: 12}
+
+
+def _sample_rows(w, n):
+    if n is None or n >= w.B:
+        return np.arange(w.B)
+    rng = np.random.default_rng(synth.seed_of(w.wid, 99))
+    return np.unique(np.concatenate([np.arange(8), rng.choice(w.B, n - 8, replace=False)]))
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_workload(orc, wid):
+    import paper_2502_06798_amd as apc
+    apc.load()
+    w = synth.WORKLOADS[wid - 1]
+    t0 = time.time()
+    say(f"workload {w.name}: generating")
+    C = synth.centres(w, "cuda")
+    e, es = synth.entries(w, "cuda", C)
+    q, qs = synth.queries(w, "cuda", C)
+    del C
+    pool = synth.latents(w, "cuda")
+    soe = synth.slot_map(w, "cuda")
+    lvl, cap, queue = synth.instances(w)
+    theta, K = synth.thresholds(w)
+    torch.cuda.synchronize()
+    say(f"  generated in {time.time() - t0:.1f}s; running the step")
+
+    cache = apc.apc_build_cache(e, es, pool, soe)
+    step = apc.MatchStep(cache, w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes)
+    if step.batch is not None:
+        step.batch.zero_()
+    step.run(q, qs)
+    torch.cuda.synchronize()
+    say(f"  step done at {time.time() - t0:.1f}s; copying to host")
+
+    ts, ti = step.top_score.cpu().numpy(), step.top_idx.cpu().numpy()
+    opt, ol, oi, os_ = (x.cpu().numpy() for x in (step.opt_level, step.out_level, step.out_inst, step.out_slot))
+    fill = step.inst_fill.cpu().numpy()[: w.n_inst]
+    eh, qh = stored_np(e), stored_np(q)
+    esh, qsh = np_or_none(es), np_or_none(qs)
+
+    # top-k on the checked rows
+    rows = _sample_rows(w, SAMPLE[wid])
+    e_sq, rc, _ = orc.row_sqnorms(w.dtype, eh, esh)
+    assert rc == 0
+    q_sq, rc, _ = orc.row_sqnorms(w.dtype, qh, qsh)
+    assert rc == 0
+    t1 = time.time()
+    rs, ri = orc.topk(w.dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, w.k,
+                      q_sq=q_sq[rows], e_sq=e_sq)
+    say(f"  reference top-k of {len(rows)} queries in {time.time() - t1:.1f}s")
+    st = check_topk(orc, w.dtype, qh, qsh, eh, esh, ts, ti, rs, ri, rows=rows, q_sq=q_sq, e_sq=e_sq)
+    say("  top-k", st)
+
+    # levels: all queries on the GPU's best; sampled against the reference best
+    lv_gpu = orc.levels(ts[:, 0].astype(np.float64), theta)
+    assert np.array_equal(opt, lv_gpu)
+    band = check_levels(orc, theta, ts[rows, 0], opt[rows], rs[:, 0], TOL[w.dtype])
+    say(f"  levels ok ({band} inside the tolerance band); histogram {np.bincount(opt, minlength=w.L + 1).tolist()}")
+
+    # assignment, bit-exact given the GPU's levels
+    r = orc.assign(opt, w.L, lvl, cap, queue)
+    assert np.array_equal(ol, r[0]) and np.array_equal(oi, r[1]) and np.array_equal(os_, r[2])
+    assert np.array_equal(fill, r[3])
+    say(f"  assignment ok: {int((ol >= 0).sum())} placed, {int((ol == opt).sum())} at their optimal level")
+
+    # gather, byte-exact given the GPU's top-1 and assignment
+    if pool is not None:
+        top1 = ti[:, 0].astype(np.int64)
+        soe_h = None if soe is None else soe.cpu().numpy()
+        cand = np.unique(top1[ol > 0])
+        slots = cand if soe_h is None else soe_h[cand]
+        cand, slots = cand[slots >= 0], slots[slots >= 0]
+        compact = np.full(w.N, -1, np.int32)
+        compact[cand] = np.arange(cand.size, dtype=np.int32)
+        pool_h = pool[torch.from_numpy(slots.astype(np.int64)).cuda()].cpu().numpy() if cand.size else \
+            np.zeros((1, w.latent_bytes), np.uint8)
+        want = np.zeros((w.n_inst * step.spi, w.latent_bytes), np.uint8)
+        h = orc.gather(top1, ol, oi, os_, compact, w.N, pool_h, w.n_inst, step.spi, want)
+        hit = step.hit.cpu().numpy()
+        assert np.array_equal(hit, h)
+        assert np.array_equal(step.batch.cpu().numpy(), want)
+        say(f"  gather ok: {int(h.sum())} latents copied")
+    say(f"  workload {w.name} done in {time.time() - t0:.1f}s")
+    cache.close()
+    del step, cache, e, es, q, qs, pool, soe
+    gc.collect()
+    torch.cuda.empty_cache()
