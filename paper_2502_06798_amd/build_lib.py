@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libapc.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "assign.hip", "gather.hip"]
+SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "assign.hip", "gather.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -35,6 +35,7 @@ hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, co
                               BuildStatus* st, hipStream_t s);
 
 // ---- similarity + top-k ----------------------------------------------------
+enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2 };
 struct MatchPlan {
     int kernel;        // kernel variant id
     int bq;            // queries per workgroup tile
@@ -50,6 +51,12 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
                         const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
                         float* top_score, int32_t* top_idx, void* ws, hipStream_t s,
                         hipEvent_t ev_start, hipEvent_t ev_stop);
+
+// streaming kernel for small batches (query factors are computed inside and
+// written to fq by the first split)
+hipError_t launch_stream(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb,
+                         const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
+                         float* fq, float* ps, int* pi, hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

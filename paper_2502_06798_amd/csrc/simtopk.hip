@@ -439,19 +439,35 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
 {
-    (void)dt; (void)d;
     MatchPlan p{};
-    p.kernel = 0;
-    p.bq = 128;
-    p.qtiles = (b + p.bq - 1) / p.bq;
-    if (p.qtiles < 1) p.qtiles = 1;
-    const int64_t ntiles = (n + 127) / 128;
-    const int target = k <= 16 ? 512 : 256;      // resident workgroups across 256 CUs
-    int64_t splits = (target + p.qtiles - 1) / p.qtiles;
-    if (splits > ntiles) splits = ntiles;
-    if (splits > 512) splits = 512;
-    if (splits < 1) splits = 1;
-    p.splits = (int)splits;
+    const int64_t rb = (int64_t)d * elem_bytes(dt);
+    const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
+    if (b <= 256 && rb <= 3072 && rb % group == 0) {
+        // small batch: query tile resident in LDS, entries streamed from HBM
+        const bool wide = k <= 16 && rb <= 1536 && dt != APC_E4M3;
+        p.kernel = wide ? KERNEL_STREAM_64 : KERNEL_STREAM_32;
+        p.bq = wide ? 64 : 32;
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        if (p.qtiles < 1) p.qtiles = 1;
+        const int64_t nblk = (n + 31) / 32;
+        int64_t splits = (256 + p.qtiles - 1) / p.qtiles;   // one workgroup per CU
+        if (splits > nblk) splits = nblk;
+        if (splits > 512) splits = 512;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+    } else {
+        p.kernel = KERNEL_TILED;
+        p.bq = 128;
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        if (p.qtiles < 1) p.qtiles = 1;
+        const int64_t ntiles = (n + 127) / 128;
+        const int target = k <= 16 ? 512 : 256;      // resident workgroups across 256 CUs
+        int64_t splits = (target + p.qtiles - 1) / p.qtiles;
+        if (splits > ntiles) splits = ntiles;
+        if (splits > 512) splits = 512;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+    }
     p.b_pad = (int64_t)p.qtiles * p.bq;
     p.off_fq = 0;
     p.off_ps = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
@@ -471,14 +487,19 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
     int* pi = reinterpret_cast<int*>(w + p.off_pi);
     const int64_t row_bytes = (int64_t)d * elem_bytes(dt);
 
-    hipError_t e = launch_row_factors(dt, b, d, q, q_scale, nullptr, 0, fq, nullptr, s);
-    if (e != hipSuccess) return e;
-    if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
-    switch (dt) {
-    case APC_F32: e = run_simtopk_k<APC_F32>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
-    case APC_F16: e = run_simtopk_k<APC_F16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
-    case APC_BF16: e = run_simtopk_k<APC_BF16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
-    default: e = run_simtopk_k<APC_E4M3>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
+    hipError_t e;
+    if (p.kernel == KERNEL_TILED) {
+        if ((e = launch_row_factors(dt, b, d, q, q_scale, nullptr, 0, fq, nullptr, s)) != hipSuccess) return e;
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        switch (dt) {
+        case APC_F32: e = run_simtopk_k<APC_F32>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
+        case APC_F16: e = run_simtopk_k<APC_F16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
+        case APC_BF16: e = run_simtopk_k<APC_BF16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
+        default: e = run_simtopk_k<APC_E4M3>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
+        }
+    } else {
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        e = launch_stream(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
     }
     if (e != hipSuccess) return e;
     if (ev_stop && (e = hipEventRecord(ev_stop, s)) != hipSuccess) return e;

@@ -90,6 +90,15 @@ CASES = [
     ("e4m3", 64, 3000, 768, 32),
     ("e4m3", 200, 1500, 112, 7),
     ("f16", 300, 129, 64, 64),
+    # streaming kernel (b <= 256, rows of whole groups of 4 x 128 bytes, 6 x 128 for e4m3)
+    ("f32", 16, 5000, 768, 5),
+    ("e4m3", 100, 2050, 768, 10),
+    ("f16", 256, 7777, 768, 10),
+    ("bf16", 3, 17, 256, 17),
+    ("f16", 5, 40, 256, 3),
+    ("e4m3", 7, 33, 768, 33),
+    ("f16", 64, 1000, 1536, 12),
+    ("f16", 200, 40000, 256, 3),
 ]
 
 
@@ -138,10 +147,11 @@ def test_match_ties_take_lower_index(apc, orc):
     c.close()
 
 
-def test_match_invalid_query_rows(apc):
-    say("match invalid query rows")
-    e, _ = make_rows(500, 32, "f16", 5)
-    q, _ = make_rows(6, 32, "f16", 6)
+@pytest.mark.parametrize("d", [32, 256])     # tiled and streaming kernels
+def test_match_invalid_query_rows(apc, d):
+    say(f"match invalid query rows d={d}")
+    e, _ = make_rows(500, d, "f16", 5)
+    q, _ = make_rows(6, d, "f16", 6)
     q[1] = 0
     q[4, 3] = float("inf")
     c = apc.apc_build_cache(e)
