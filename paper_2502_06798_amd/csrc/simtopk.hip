@@ -442,7 +442,21 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     MatchPlan p{};
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
-    if (b <= 256 && rb <= 3072 && rb % group == 0) {
+    const int qsb = qstat_queries(dt, rb);
+    if (qsb > 0 && k <= 16 && b <= 2 * qsb) {
+        // small batch, 16-bit or e4m3 rows: queries in registers, each cache row
+        // staged through LDS once per workgroup
+        p.kernel = KERNEL_QSTAT;
+        p.bq = qsb;
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        if (p.qtiles < 1) p.qtiles = 1;
+        const int64_t nblk = (n + 31) / 32;
+        int64_t splits = 256 / p.qtiles;                     // one workgroup per CU
+        if (splits >= 8) splits &= ~(int64_t)7;              // query tiles of a split share an XCD
+        if (splits > nblk) splits = nblk >= 8 ? (nblk & ~(int64_t)7) : nblk;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+    } else if (b <= 256 && rb <= 3072 && rb % group == 0) {
         // small batch: query tile resident in LDS, entries streamed from HBM
         const bool wide = k <= 16 && rb <= 1536 && dt != APC_E4M3;
         p.kernel = wide ? KERNEL_STREAM_64 : KERNEL_STREAM_32;
@@ -497,6 +511,9 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         case APC_BF16: e = run_simtopk_k<APC_BF16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         default: e = run_simtopk_k<APC_E4M3>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         }
+    } else if (p.kernel == KERNEL_QSTAT) {
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        e = launch_qstat(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_stream(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);

@@ -90,7 +90,8 @@ CASES = [
     ("e4m3", 64, 3000, 768, 32),
     ("e4m3", 200, 1500, 112, 7),
     ("f16", 300, 129, 64, 64),
-    # streaming kernel (b <= 256, rows of whole groups of 4 x 128 bytes, 6 x 128 for e4m3)
+    # streaming kernel (b <= 256, rows of whole groups of 4 x 128 bytes, 6 x 128 for e4m3;
+    # float rows, or k > 16, or row sizes the query-stationary kernel is not built for)
     ("f32", 16, 5000, 768, 5),
     ("e4m3", 100, 2050, 768, 10),
     ("f16", 256, 7777, 768, 10),
@@ -99,6 +100,16 @@ CASES = [
     ("e4m3", 7, 33, 768, 33),
     ("f16", 64, 1000, 1536, 12),
     ("f16", 200, 40000, 256, 3),
+    ("bf16", 100, 3000, 768, 20),
+    # query-stationary kernel (k <= 16; f16/bf16 rows of 512, 1024, 1536 bytes,
+    # e4m3 rows of 512 or 768 bytes)
+    ("f16", 256, 50000, 768, 10),
+    ("bf16", 129, 3001, 768, 16),
+    ("e4m3", 300, 9000, 768, 10),
+    ("f16", 1, 31, 768, 5),
+    ("f16", 40, 100, 512, 7),
+    ("e4m3", 5, 70000, 512, 16),
+    ("bf16", 512, 20000, 256, 8),
 ]
 
 
