@@ -68,25 +68,41 @@ def alg_bytes(w):
     return w.N * w.d * eb + 4 * w.N + w.B * (w.d * eb + scale) + 8 * w.B * w.k
 
 
-def cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta, n_queries):
-    """The float64 reference on the first n_queries queries against the full cache."""
-    import numpy as np
+def cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta, n_queries, min_seconds=10.0):
+    """The float64 reference on the first n_queries queries against the full cache,
+    repeated until at least min_seconds of CPU work have been timed."""
     from oracle import oracle
     from paper_2502_06798_amd.synth import host_view
     eh, qh = host_view(e), host_view(q[:n_queries])
     esh, qsh = host_view(es), host_view(None if qs is None else qs[:n_queries])
     e_sq, _, _ = oracle.row_sqnorms(w.dtype, eh, esh)
-    t0 = time.perf_counter()
-    q_sq, _, _ = oracle.row_sqnorms(w.dtype, qh, qsh)
-    ts, ti = oracle.topk(w.dtype, qh, qsh, eh, esh, w.k, q_sq=q_sq, e_sq=e_sq)
-    lv = oracle.levels(ts[:, 0], theta)
-    oracle.assign(lv, w.L, lvl, cap, queue)
-    dt = time.perf_counter() - t0
-    return {"value": round(n_queries / dt, 3), "unit": "prompts/s", "cores": oracle.max_threads(),
+    reps, dt = 0, 0.0
+    while dt < min_seconds:
+        t0 = time.perf_counter()
+        q_sq, _, _ = oracle.row_sqnorms(w.dtype, qh, qsh)
+        ts, ti = oracle.topk(w.dtype, qh, qsh, eh, esh, w.k, q_sq=q_sq, e_sq=e_sq)
+        lv = oracle.levels(ts[:, 0], theta)
+        oracle.assign(lv, w.L, lvl, cap, queue)
+        dt += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(reps * n_queries / dt, 3), "unit": "prompts/s", "cores": oracle.max_threads(),
             "kind": "oracle",
-            "sample": f"{n_queries} of {w.B} queries of {w.name} against all {w.N} entries "
+            "sample": f"{reps} x {n_queries} of {w.B} queries of {w.name} against all {w.N} entries "
                       f"(top-{w.k}, levels, assignment), {dt:.2f} s; the entry norms are "
                       "computed once outside the timed part"}
+
+
+def copy_probe(mib, reps=5):
+    """A plain device copy of known size (calibrates the HBM byte counters)."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "reps": reps}), flush=True)
 
 
 def main():
@@ -97,7 +113,10 @@ def main():
     ap.add_argument("--workload", default="b256_n100k_d768_f16")
     ap.add_argument("--copies", type=int, default=0, help="cache copies rotated per step (0 = auto)")
     ap.add_argument("--cpu-queries", type=int, default=256)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -110,8 +129,11 @@ def main():
     import paper_2502_06798_amd as apc
     from paper_2502_06798_amd import synth
 
-    apc.load()
     torch.cuda.set_device(0)
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
+    apc.load()
     w = synth.BY_NAME[args.workload]
     log(f"generating {w.name}")
     C = synth.centres(w, "cuda")
@@ -188,7 +210,7 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU reference")
         out["cpu_baseline"] = cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta,
-                                           min(args.cpu_queries, w.B))
+                                           min(args.cpu_queries, w.B), args.cpu_seconds)
     for c in caches:
         c.close()
     print(json.dumps(out), flush=True)
