@@ -14,12 +14,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libapc.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qstat.hip", "assign.hip", "gather.hip"]
+SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qstat.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "assign.hip", "gather.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # no packed fp32 instructions: hipcc would otherwise form them from plain float code
-         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # MFMA results in VGPRs: no copies of the accumulators between register files
+         "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _compile(src: str) -> str:

@@ -23,7 +23,7 @@ struct apc_cache {
     int64_t n_slots;
     int64_t latent_bytes;
     const int32_t* slot_of_entry;
-    float* fe;          // owned: n row factors, padded with zeros to a multiple of 256
+    float* fe;          // owned: row factors and group bounds (layout in apc_internal.h)
     int device;
 };
 
@@ -145,10 +145,10 @@ apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, 
 
     apc_cache* c = new (std::nothrow) apc_cache{};
     if (!c) return fail(APC_E_NOMEM, "apc_build_cache: host allocation failed");
-    const int64_t n_pad = (n + 255) / 256 * 256;
+    const int64_t n_pad = apc::factor_pad(n);
     apc::BuildStatus* dst = nullptr;
     apc::BuildStatus hst{};
-    if ((e = hipMalloc(&c->fe, sizeof(float) * n_pad)) != hipSuccess) {
+    if ((e = hipMalloc(&c->fe, sizeof(float) * apc::factor_floats(n))) != hipSuccess) {
         delete c;
         return fail(APC_E_NOMEM, "apc_build_cache: hipMalloc of %lld row factors: %s", (long long)n,
                     hipGetErrorString(e));
@@ -166,6 +166,7 @@ apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, 
     if ((e = hipMemsetAsync(c->fe + n, 0, sizeof(float) * (n_pad - n), s)) != hipSuccess ||
         (e = hipMemcpyAsync(dst, &hst, sizeof hst, hipMemcpyHostToDevice, s)) != hipSuccess ||
         (e = apc::launch_row_factors(dt, n, d, emb, row_scale, slot_of_entry, n_slots, c->fe, dst, s)) != hipSuccess ||
+        (e = apc::launch_group_bounds(c->fe, n, n_pad, c->fe + n_pad, s)) != hipSuccess ||
         (e = hipMemcpyAsync(&hst, dst, sizeof hst, hipMemcpyDeviceToHost, s)) != hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess) {
         cleanup();

@@ -34,15 +34,22 @@ hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, co
                               const int32_t* slot_of_entry, int64_t n_slots, float* f,
                               BuildStatus* st, hipStream_t s);
 
+// factor layout of a cache: n_pad = n rounded up to a multiple of 256 factors
+// (zeros past n), then n_pad / 64 groups of {max, min, 0, 0} over each 64-row
+// group's factors
+__host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }
+__host__ __device__ inline int64_t factor_floats(int64_t n) { return factor_pad(n) + factor_pad(n) / 16; }
+hipError_t launch_group_bounds(const float* f, int64_t n, int64_t n_pad, float* fb, hipStream_t s);
+
 // ---- similarity + top-k ----------------------------------------------------
-enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QSTAT = 3 };
+enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QSTAT = 3, KERNEL_QS = 4 };
 struct MatchPlan {
     int kernel;        // kernel variant id
     int bq;            // queries per workgroup tile
     int qtiles;        // ceil(b / bq)
     int splits;        // workgroups along the entries per query tile
     int64_t b_pad;     // qtiles * bq
-    size_t off_fq, off_ps, off_pi, bytes;   // workspace layout
+    size_t off_fq, off_gt, off_ps, off_pi, bytes;   // workspace layout
 };
 MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k);
 
@@ -65,6 +72,18 @@ int qstat_queries(int dt, int64_t row_bytes);
 hipError_t launch_qstat(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb,
                         const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
                         float* fq, float* ps, int* pi, hipStream_t s);
+
+// query-stationary kernel for 16-bit and e4m3 rows of 512..1536 bytes (k <= qs_max_k()):
+// queries in VGPRs, cache rows through an LDS ring, per-query bounds shared
+// between workgroups.  qs_queries gives the queries per workgroup (0: not built).
+int qs_queries(int dt, int64_t row_bytes);
+int qs_max_k();
+// query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
+hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
+                        float* fq, int* gthr, hipStream_t s);
+hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
+                     const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
+                     hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

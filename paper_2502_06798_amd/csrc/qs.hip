@@ -1,0 +1,80 @@
+// Query preparation for the query-stationary kernel and its dispatch by
+// storage type (the kernel itself is in qs_kernel.h, instantiated per type).
+#include "qs_kernel.h"
+
+namespace apc {
+namespace {
+
+// query factors f = 1/|q| (NaN for rows that cannot be matched: non-finite,
+// zero norm, bad e4m3 scale, or padding) and reset global bounds, one
+// wavefront per padded query row
+template <int DT>
+__global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, const float* __restrict__ q_scale,
+                                                int32_t b, int64_t b_pad, int64_t row_bytes,
+                                                float* __restrict__ fq, int* __restrict__ gthr)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= b_pad) return;
+    float ss = 0.f;
+    bool bad = false;
+    if (r < b) {
+        const uint8_t* row = qry + r * row_bytes;
+        for (int64_t off = (int64_t)lane * 16; off < row_bytes; off += 64 * 16)
+            sumsq16<DT>(*reinterpret_cast<const uint4*>(row + off), ss, bad);
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    bad = __any(bad);
+    if (lane != 0) return;
+    bool ok = r < b && !bad && __builtin_isfinite(ss) && ss > 0.f;
+    if (ok && q_scale) {
+        const float sc = q_scale[r];
+        ok = __builtin_isfinite(sc) && sc > 0.f;
+    }
+    fq[r] = ok ? 1.0f / __builtin_sqrtf(ss) : qnan();
+    gthr[r] = q2_key(neg_inf());
+}
+
+}  // namespace
+
+int qs_queries(int dt, int64_t row_bytes)
+{
+    switch (dt) {
+    case APC_F16: return q2_queries<APC_F16>(row_bytes);
+    case APC_BF16: return q2_queries<APC_BF16>(row_bytes);
+    case APC_E4M3: return q2_queries<APC_E4M3>(row_bytes);
+    default: return 0;
+    }
+}
+
+int qs_max_k() { return Q2_KMAX; }
+
+hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
+                        float* fq, int* gthr, hipStream_t s)
+{
+    const dim3 grid((unsigned)((b_pad + 3) / 4)), block(256);
+    const uint8_t* qp = static_cast<const uint8_t*>(q);
+    switch (dt) {
+    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    default: k_qprep<APC_F32><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
+                     const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
+                     hipStream_t s)
+{
+    const int64_t rb = (int64_t)d * elem_bytes(dt);
+    switch (dt) {
+    case APC_F16: return launch_qs_f16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_BF16: return launch_qs_bf16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_E4M3: return launch_qs_e4m3(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace apc

@@ -1,0 +1,500 @@
+// Query-stationary similarity + exact top-k for 16-bit and e4m3 rows.
+//
+// Grid: splits x query tiles.  A workgroup of four wavefronts (one per SIMD)
+// owns a tile of 4 x MQ x 32 queries and a contiguous range of cache entries
+// (its split).  Each wavefront keeps its MQ x 32 query rows in VGPRs for its
+// whole life, as the B operands of 32x32 MFMAs (lane l supplies query row
+// l % 32; half h = l / 32 supplies bytes [64h, 64h + 64) of every 128-byte
+// chunk of d).  Cache rows stream through an LDS ring in stages of 64 rows x
+// 256 bytes, loaded straight from global memory into LDS (no VGPRs held by
+// loads in flight); a 16-byte unit of a row sits at unit ^ (row % 16), so the
+// A-operand reads (lane = row) are free of bank conflicts.  One barrier per
+// stage makes the stage visible to the four wavefronts, which all use it.
+// The 64 rows of a stage form two 32-row blocks, so each wavefront runs
+// 2 x MQ independent accumulation chains; every score is the sum over all of
+// d in float32, in the same order whatever the split or tile.
+//
+// Top-k, per wavefront (its queries are its own, so no cross-wave sync):
+//  * after a group of 64 entries, each lane scales its 32 products by the
+//    entry factors and takes their maximum; clamp(max * f_q) is exactly the
+//    best score among them (scaling by f_q > 0 and clamping are monotone), so
+//    only lanes whose maximum reaches the filter threshold look further;
+//  * the filter threshold is the larger of the query's own k-th pair (its
+//    list in LDS) and a per-query global bound shared by all workgroups
+//    through atomicMax: a published value is the k-th best score of some
+//    subset of the entries, so k entries score at least that much and any
+//    entry below it cannot be in the top-k (ties are kept);
+//  * passing pairs replace the worst pair of the query's list (first filling
+//    empty slots); the two lanes of a query take turns, lane half 0 first.
+// At the end each query's list is sorted by rank (score desc, index asc) and
+// written as the split's partial list; k_topk_merge merges the splits.
+#pragma once
+
+#include <type_traits>
+
+#include "topk_wg.h"
+
+namespace apc {
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int Q2_NW = 4;                   // wavefronts per workgroup
+constexpr int Q2_NT = Q2_NW * 64;
+constexpr int Q2_SB = 256;                 // bytes of each row per stage
+constexpr int Q2_GR = 64;                  // rows per stage and per group (two 32-row blocks)
+constexpr int Q2_STAGE = Q2_GR * Q2_SB;    // 16 KB
+constexpr int Q2_LPW = Q2_STAGE / 1024 / Q2_NW;   // row loads per wavefront per stage
+constexpr int Q2_FR = 8;                   // ring of per-group side data
+constexpr int Q2_KMAX = 32;                // largest k
+
+// s_waitcnt immediate: at most n vector-memory operations outstanding
+constexpr int q2_vmcnt(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16 l.  An asm statement, so that the compiler does not make every
+// later LDS read wait for all loads in flight; the kernel counts them itself.
+__device__ inline void q2_dma16(const void* g, uint32_t lds)
+{
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+
+// the same, coherent across the device (values other workgroups update with
+// device-scope atomics; plain loads could hit a stale line in this XCD's L2)
+__device__ inline void q2_dma16_fresh(const void* g, uint32_t lds)
+{
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off sc1" ::"v"(g), "{m0}"(lds) : "memory");
+}
+
+// order-preserving int image of a float (for atomicMax on scores)
+__device__ inline int q2_key(float f)
+{
+    const int i = __float_as_int(f);
+    return i >= 0 ? i : i ^ 0x7fffffff;
+}
+__device__ inline float q2_unkey(int k) { return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff); }
+
+// fire-and-forget atomic max (no return value, nothing to wait for)
+__device__ inline void q2_atomic_max(int* p, int v)
+{
+    asm volatile("global_atomic_smax %0, %1, off" ::"v"(p), "v"(v) : "memory");
+}
+
+template <int DT> struct Q2Op { typedef uint4 Step; static constexpr int UPS = 1; };
+template <> struct Q2Op<APC_E4M3> { typedef i32x8 Step; static constexpr int UPS = 2; };
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>)
+template <int N, int I = 0, class Fn>
+__device__ inline __attribute__((always_inline)) void static_for(Fn&& f)
+{
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
+    }
+}
+
+struct Q2Pair {
+    float s;
+    int i;
+};
+
+template <int DT, int RB, int MQ>
+struct Q2Cfg {
+    typedef typename Q2Op<DT>::Step Step;
+    static constexpr int UPS = Q2Op<DT>::UPS;         // 16-byte units per MFMA step
+    static constexpr int SPG = RB / Q2_SB;            // stages per group
+    static constexpr int SST = Q2_SB / 32 / UPS;      // MFMA steps per stage (per block)
+    static constexpr int QST = RB / 32 / UPS;         // steps of a query row held by a lane
+    static constexpr int BQW = MQ * 32;               // queries per wavefront
+    static constexpr int BQ = Q2_NW * BQW;            // queries per workgroup
+    static constexpr int NS = MQ == 1 ? 7 : 5;        // stages in the LDS ring
+    static_assert(RB % Q2_SB == 0 && SPG >= 2, "rows must be at least two whole stages");
+    static_assert(SPG <= 6, "wait_stage covers up to six stages per group");
+    static_assert(Q2_STAGE % (1024 * Q2_NW) == 0, "stage loads split evenly over the wavefronts");
+    // vector-memory operations a wavefront issues after stage t's row loads and
+    // before it waits for stage t (j = t % SPG), in steady state: the side
+    // loads (entry factors, global thresholds) of every group start in
+    // [t, t + NS - 2], and the row loads of stages t + 1 .. t + NS - 2
+    static constexpr int after(int j)
+    {
+        const int starts = j == 0 ? (NS - 2) / SPG + 1 : (j + NS - 2) / SPG;
+        return (NS - 2) * Q2_LPW + 2 * starts;
+    }
+    __device__ static void wait_stage(int j)
+    {
+        switch (j) {
+        case 0: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(0))); break;
+        case 1: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(1))); break;
+        case 2: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(2))); break;
+        case 3: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(3))); break;
+        case 4: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(4))); break;
+        default: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(5))); break;
+        }
+    }
+    struct Smem {
+        uint8_t e[NS * Q2_STAGE];
+        float fe[Q2_FR][Q2_GR + 4];             // entry factors of a group, then {max, min, -, -}
+        int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
+        Q2Pair lst[Q2_NW][Q2_KMAX][BQW];        // per-wavefront lists, slot-major
+    };
+};
+
+template <int DT>
+__device__ inline void q2_mma(f32x16& c, const typename Q2Op<DT>::Step a, const typename Q2Op<DT>::Step b)
+{
+    if constexpr (DT == APC_F16)
+        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    else if constexpr (DT == APC_BF16)
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    else
+        c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// worst pair of a list of k (the one every other pair comes before): all
+// KR slots are read at once, slots >= k count as the best possible pair, and
+// a tree of comparisons picks the worst
+template <int KR, int BQW>
+__device__ inline void q2_worst(const Q2Pair (*lst)[BQW], int col, int k, float& ws, int& wi, int& wp)
+{
+    float xs[KR];
+    int xi[KR], xp[KR];
+#pragma unroll
+    for (int p = 0; p < KR; ++p) {
+        const Q2Pair x = lst[p][col];
+        xs[p] = p < k ? x.s : __builtin_huge_valf();
+        xi[p] = p < k ? x.i : -1;
+        xp[p] = p;
+    }
+#pragma unroll
+    for (int w = 1; w < KR; w *= 2)
+#pragma unroll
+        for (int p = 0; p + w < KR; p += 2 * w) {
+            const bool tk = before(xs[p], xi[p], xs[p + w], xi[p + w]);   // p + w is the worse
+            xs[p] = tk ? xs[p + w] : xs[p];
+            xi[p] = tk ? xi[p + w] : xi[p];
+            xp[p] = tk ? xp[p + w] : xp[p];
+        }
+    ws = xs[0];
+    wi = xi[0];
+    wp = xp[0];
+}
+
+// grid: workgroup id -> (split, query tile).  With a grid that is a multiple
+// of 8, consecutive linear indices go to the same XCD (workgroups are dealt
+// round-robin over the 8 XCDs), so the query tiles of a split run side by
+// side on one XCD and share its L2.
+template <int DT, int RB, int MQ>
+__global__ __launch_bounds__(Q2_NT) void k_qs(
+    const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
+    const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
+    int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i)
+{
+    typedef Q2Cfg<DT, RB, MQ> C;
+    typedef typename C::Step Step;
+    constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
+    __shared__ typename C::Smem sm;
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    const int grid = (int)gridDim.x, work = splits * qtiles;
+    const int lin = (grid & 7) == 0 ? (int)(blockIdx.x & 7) * (grid >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
+    if (lin >= work) return;                                       // whole workgroup: uniform
+    const int split = lin / qtiles, qtile = lin % qtiles;
+    const int64_t q0w = (int64_t)qtile * C::BQ + wave * BQW;      // this wavefront's first query
+    const bool live = q0w < b;                                     // uniform per wavefront
+
+    const int64_t ngr = (n + Q2_GR - 1) / Q2_GR;                   // 64-row groups of the cache
+    const float* fb = fe + factor_pad(n);                          // per-group factor bounds
+    const int64_t g_begin = ngr * split / splits;
+    const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
+    const int T = ng * SPG;                                        // stages of this split
+
+    // ---- stage loads: wavefront w fills rows [16w, 16w + 16) of a stage ----
+    const uint32_t lds_e = (uint32_t)(size_t)(lds_void*)sm.e;
+    const uint32_t lds_fe = (uint32_t)(size_t)(lds_void*)&sm.fe[0][0];
+    const uint32_t lds_gt = (uint32_t)(size_t)(lds_void*)&sm.gthr[0][0][0];
+    int lrow[Q2_LPW], loff[Q2_LPW];
+#pragma unroll
+    for (int i = 0; i < Q2_LPW; ++i) {
+        lrow[i] = wave * (Q2_GR / Q2_NW) + i * 4 + (lane >> 4);
+        loff[i] = ((lane & 15) ^ (lrow[i] & 15)) * 16;             // logical unit stored at unit lane % 16
+    }
+    // row pointers of the group being issued (groups are issued in order); a
+    // stage j of the group adds j * 256 to them (not through the load's offset
+    // field: for loads into LDS that offset moves the LDS address too)
+    const uint8_t* rowp[Q2_LPW];
+    auto issue = [&](int gi, auto jc) __attribute__((always_inline)) {                            // stage j of group gi
+        constexpr int j = decltype(jc)::value;
+        const int64_t e0 = (g_begin + gi) * Q2_GR;
+        if constexpr (j == 0) {
+            const int64_t last = n - 1 - e0;                       // last valid row of the group
+#pragma unroll
+            for (int i = 0; i < Q2_LPW; ++i) {
+                const int64_t row = lrow[i] < last ? lrow[i] : last;
+                rowp[i] = emb + (e0 + row) * RB + loff[i];
+            }
+        }
+        const int t = gi * SPG + j;
+        const uint32_t sbase = lds_e + (uint32_t)(t % NS) * Q2_STAGE;
+#pragma unroll
+        for (int i = 0; i < Q2_LPW; ++i)
+            q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
+                                              sbase + (uint32_t)(wave * (Q2_GR / Q2_NW) + i * 4) * Q2_SB));
+        if constexpr (j == 0) {
+            // the group's 64 entry factors (padded to whole groups) with its
+            // factor bounds, and this wavefront's global bounds: one load each,
+            // lanes beyond the data idle
+            const float* fsrc = lane < Q2_GR / 4 ? fe + e0 + lane * 4 : fb + (g_begin + gi) * 4;
+            if (lane <= Q2_GR / 4) q2_dma16(fsrc, lds_fe + (uint32_t)(gi % Q2_FR) * ((Q2_GR + 4) * 4));
+            const int gl = lane < BQW / 4 ? lane : 0;
+            if (lane < BQW / 4)
+                q2_dma16_fresh(gthr + q0w + gl * 4,
+                               lds_gt + (uint32_t)(((gi % Q2_FR) * Q2_NW + wave) * BQW * 4));
+        }
+    };
+    // stage s = t0 + d of the schedule, with t0 = gi0 * SPG + j0 (j0, d compile-time)
+    auto issue_ahead = [&](int gi0, auto j0c, auto dc) __attribute__((always_inline)) {
+        constexpr int js = (decltype(j0c)::value + decltype(dc)::value) % SPG;
+        constexpr int dg = (decltype(j0c)::value + decltype(dc)::value) / SPG;
+        issue(gi0 + dg, std::integral_constant<int, js>{});
+    };
+    static_for<NS - 1>([&](auto sc) __attribute__((always_inline)) {
+        if (decltype(sc)::value < T) issue_ahead(0, std::integral_constant<int, 0>{}, sc);
+    });
+
+    // ---- queries into VGPRs, factors, empty lists ----
+    Step qv[C::QST][MQ];
+    float fq[MQ];
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) {
+        const int64_t qg = q0w + mq * 32 + r32;
+        const uint8_t* qrow = qry + (qg < b ? qg : 0) * RB + h * 64;
+#pragma unroll
+        for (int s = 0; s < C::QST; ++s) {
+            const int u = s * UPS;
+            qv[s][mq] = *reinterpret_cast<const Step*>(qrow + (u / 4) * 128 + (u % 4) * 16);
+        }
+        fq[mq] = fq_ws[qg];                          // NaN for rows that cannot be matched
+    }
+    Q2Pair(*lst)[BQW] = sm.lst[wave];
+    for (int i = lane; i < Q2_KMAX * BQW; i += 64) lst[i / BQW][i % BQW] = Q2Pair{neg_inf(), IDX_NONE};
+    float Ts[MQ];      // worst pair of the query's list (-inf, none while it has empty slots)
+    int Ti[MQ], Wp[MQ], fill[MQ];
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) {
+        Ts[mq] = neg_inf();
+        Ti[mq] = IDX_NONE;
+        Wp[mq] = 0;
+        fill[mq] = 0;
+    }
+
+    f32x16 acc[MQ][2];
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq)
+#pragma unroll
+        for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
+
+    for (int gi = 0; gi < ng; ++gi) {
+        static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
+            constexpr int j = decltype(jc)::value;
+            const int t = gi * SPG + j;
+            if (t + NS - 2 < T) C::wait_stage(j);
+            else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
+            __syncthreads();
+            if (t + NS - 1 < T)                                    // into the slot stage t - 1 used
+                issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
+            if (!live) return;
+            const uint8_t* sb = sm.e + (t % NS) * Q2_STAGE + r32 * Q2_SB;
+            Step a[2][SST];
+#pragma unroll
+            for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+                for (int ss = 0; ss < SST; ++ss) {
+                    const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
+                    const int lu = cl * 8 + h * 4 + sp;                  // logical 16-byte unit
+                    const uint8_t* rp = sb + eb * 32 * Q2_SB;
+                    if constexpr (UPS == 1) {
+                        a[eb][ss] = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
+                    } else {
+                        const uint4 x0 = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
+                        const uint4 x1 = *reinterpret_cast<const uint4*>(rp + (((lu + 1) ^ (r32 & 15)) * 16));
+                        a[eb][ss] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
+                                         (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+                    }
+                }
+#pragma unroll
+            for (int ss = 0; ss < SST; ++ss)
+#pragma unroll
+                for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+                    for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[eb][ss], qv[j * SST + ss][mq]);
+            // reads ahead of the MFMAs (otherwise each read is paired with its MFMA
+            // and every read's latency is waited out)
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * SST * UPS, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * SST * MQ, 0);
+        });
+        if (!live) continue;
+
+        // ---- epilogue of the group ----
+        // lane (h, c) holds for query c the rows 8 g + 4 h + i (g, i < 4) of each
+        // block; quad p = 4 eb + g groups its four rows i
+        const int64_t e0 = (g_begin + gi) * Q2_GR;
+        const bool whole = e0 + Q2_GR <= n;
+        const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
+        // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f)
+        const float* fr = sm.fe[gi % Q2_FR];
+        const float fmx = fr[Q2_GR], fmn = fr[Q2_GR + 1];
+        float G[MQ], F[MQ];
+        bool pass[MQ];
+        bool any_pass = false;
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) {
+            G[mq] = q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]);
+            float am = acc[mq][0][0];
+#pragma unroll
+            for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+                for (int r = (eb == 0 ? 1 : 0); r < 16; ++r) am = __builtin_fmaxf(am, acc[mq][eb][r]);
+            const float ub = am * (am >= 0.f ? fmx : fmn);
+            F[mq] = __builtin_fmaxf(Ts[mq], G[mq]);
+            pass[mq] = fq[mq] == fq[mq] && clamp1(ub * fq[mq]) >= F[mq];   // NaN f_q: row not matched
+            any_pass |= pass[mq];
+        }
+        if (__builtin_amdgcn_ballot_w64(any_pass)) {
+#pragma unroll
+            for (int mq = 0; mq < MQ; ++mq) {
+                // exact products, and the quads whose best score reaches the filter
+                uint32_t qbits = 0;
+                if (pass[mq]) {
+#pragma unroll
+                    for (int p = 0; p < 8; ++p) {
+                        const int eb = p >> 2, g = p & 3;
+                        const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                        const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
+                        float qm = neg_inf();
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float v = acc[mq][eb][4 * g + i] * fv[i];
+                            acc[mq][eb][4 * g + i] = v;
+                            if (whole || 32 * eb + 8 * g + i < lim64) qm = __builtin_fmaxf(qm, v);
+                        }
+                        qbits |= (uint32_t)(qm > neg_inf() && clamp1(qm * fq[mq]) >= F[mq]) << p;
+                    }
+                }
+                const int col = mq * 32 + r32;
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    uint32_t mine = h == h2 ? qbits : 0u;
+                    while (__builtin_amdgcn_ballot_w64(mine != 0)) {
+                        const bool act = mine != 0;
+                        const int p = act ? __builtin_ctz(mine) : 0;
+                        mine &= mine - 1;
+                        // the quad's four products (select over the eight quads)
+                        float x[4];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            float v = acc[mq][0][i];
+#pragma unroll
+                            for (int pp = 1; pp < 8; ++pp) v = p == pp ? acc[mq][pp >> 2][4 * (pp & 3) + i] : v;
+                            x[i] = v;
+                        }
+                        const int eb = p >> 2, g = p & 3;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float s = clamp1(x[i] * fq[mq]);
+                            const int e = (int)(e0 + 32 * eb + 8 * g + 4 * h + i);
+                            const bool ok = act && (whole || 32 * eb + 8 * g + i < lim64) && s >= G[mq] &&
+                                            before(s, e, Ts[mq], Ti[mq]);
+                            if (ok) {
+                                lst[Wp[mq]][col] = Q2Pair{s, e};
+                                if (fill[mq] < k - 1) {
+                                    fill[mq] += 1;
+                                    Wp[mq] = fill[mq];
+                                } else {
+                                    fill[mq] = k;
+                                    if (k <= 16) q2_worst<16>(lst, col, k, Ts[mq], Ti[mq], Wp[mq]);
+                                    else q2_worst<Q2_KMAX>(lst, col, k, Ts[mq], Ti[mq], Wp[mq]);
+                                }
+                            }
+                        }
+                    }
+                    // the other half of the query continues from this half's list state
+                    const int src = h2 * 32 + r32;
+                    Ts[mq] = __shfl(Ts[mq], src, 64);
+                    Ti[mq] = __shfl(Ti[mq], src, 64);
+                    Wp[mq] = __shfl(Wp[mq], src, 64);
+                    fill[mq] = __shfl(fill[mq], src, 64);
+                }
+                // publish a raised k-th score for the other workgroups
+                if (h == 0 && fill[mq] == k && Ts[mq] > G[mq]) {
+                    const int64_t qg = q0w + col;
+                    q2_atomic_max(gthr + qg, q2_key(Ts[mq]));
+                }
+            }
+        }
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq)
+#pragma unroll
+            for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
+    }
+
+    if (!live) return;
+    // ---- each query's list in rank order as the split's partial list ----
+    // lane half h ranks slots h, h + 2, ...; equal pairs (empty slots) are
+    // ordered by slot so that every rank is written once
+    __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) {
+        const int col = mq * 32 + r32;
+        const int64_t qg = q0w + col;
+        const int64_t o = ((int64_t)split * b_pad + qg) * k;
+        for (int p = h; p < k; p += 2) {
+            const Q2Pair x = lst[p][col];
+            int rank = 0;
+            for (int p2 = 0; p2 < k; ++p2) {
+                const Q2Pair y = lst[p2][col];
+                rank += before(y.s, y.i, x.s, x.i) || (y.s == x.s && y.i == x.i && p2 < p);
+            }
+            part_s[o + rank] = x.s;
+            part_i[o + rank] = x.i;
+        }
+    }
+}
+
+template <int DT, int RB, int MQ>
+hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
+                  int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+{
+    const int work = p.splits * p.qtiles;
+    const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
+    k_qs<DT, RB, MQ><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
+                                            static_cast<const uint8_t*>(q), fq, gthr, b, k, p.splits,
+                                            p.qtiles, p.b_pad, ps, pi);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// shape of the query-stationary kernel for a row size (0 = not built)
+template <int DT>
+constexpr int q2_queries(int64_t row_bytes)
+{
+    if constexpr (DT == APC_E4M3)
+        return row_bytes == 1024 || row_bytes == 768 || row_bytes == 512 ? Q2Cfg<DT, 512, 2>::BQ : 0;
+    else
+        return row_bytes == 1536 ? Q2Cfg<DT, 1536, 1>::BQ
+             : row_bytes == 1024 || row_bytes == 768 || row_bytes == 512 ? Q2Cfg<DT, 512, 2>::BQ : 0;
+}
+
+hipError_t launch_qs_f16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
+                         const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+hipError_t launch_qs_bf16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
+                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+hipError_t launch_qs_e4m3(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
+                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+
+}  // namespace apc

@@ -442,8 +442,21 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     MatchPlan p{};
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
+    const int q2b = qs_queries(dt, rb);
     const int qsb = qstat_queries(dt, rb);
-    if (qsb > 0 && k <= 16 && b <= 2 * qsb) {
+    if (q2b > 0 && k <= qs_max_k()) {
+        // 16-bit or e4m3 rows: queries in VGPRs, cache rows through LDS, one
+        // workgroup per CU; the query tiles of a split share an XCD
+        p.kernel = KERNEL_QS;
+        p.bq = q2b;
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        if (p.qtiles < 1) p.qtiles = 1;
+        const int64_t ngr = (n + 63) / 64;
+        int64_t splits = p.qtiles >= 256 ? 1 : 256 / p.qtiles;
+        if (splits > ngr) splits = ngr;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+    } else if (qsb > 0 && k <= 16 && b <= 2 * qsb) {
         // small batch, 16-bit or e4m3 rows: queries in registers, each cache row
         // staged through LDS once per workgroup
         p.kernel = KERNEL_QSTAT;
@@ -484,7 +497,8 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     }
     p.b_pad = (int64_t)p.qtiles * p.bq;
     p.off_fq = 0;
-    p.off_ps = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
+    p.off_gt = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
+    p.off_ps = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
     p.bytes = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
     return p;
@@ -511,6 +525,11 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         case APC_BF16: e = run_simtopk_k<APC_BF16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         default: e = run_simtopk_k<APC_E4M3>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         }
+    } else if (p.kernel == KERNEL_QS) {
+        int* gt = reinterpret_cast<int*>(w + p.off_gt);
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, s)) != hipSuccess) return e;
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        e = launch_qs(p, dt, n, d, emb, fe, q, fq, gt, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QSTAT) {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qstat(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
