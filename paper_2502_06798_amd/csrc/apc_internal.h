@@ -73,10 +73,10 @@ hipError_t launch_qstat(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
                         const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
                         float* fq, float* ps, int* pi, hipStream_t s);
 
-// query-stationary kernel for 16-bit and e4m3 rows of 512..1536 bytes (k <= qs_max_k()):
+// query-stationary kernel for 16-bit and e4m3 rows of 512, 768, 1024 or 1536 bytes (k <= qs_max_k()):
 // queries in VGPRs, cache rows through an LDS ring, per-query bounds shared
 // between workgroups.  qs_queries gives the queries per workgroup (0: not built).
-int qs_queries(int dt, int64_t row_bytes);
+int qs_queries(int dt, int64_t row_bytes, int k);
 int qs_max_k();
 // query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,

@@ -38,14 +38,9 @@ __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, 
 
 }  // namespace
 
-int qs_queries(int dt, int64_t row_bytes)
+int qs_queries(int dt, int64_t row_bytes, int k)
 {
-    switch (dt) {
-    case APC_F16: return q2_queries<APC_F16>(row_bytes);
-    case APC_BF16: return q2_queries<APC_BF16>(row_bytes);
-    case APC_E4M3: return q2_queries<APC_E4M3>(row_bytes);
-    default: return 0;
-    }
+    return dt == APC_F16 || dt == APC_BF16 || dt == APC_E4M3 ? q2_queries(row_bytes, k) : 0;
 }
 
 int qs_max_k() { return Q2_KMAX; }

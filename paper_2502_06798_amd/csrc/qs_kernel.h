@@ -47,6 +47,7 @@ constexpr int Q2_STAGE = Q2_GR * Q2_SB;    // 16 KB
 constexpr int Q2_LPW = Q2_STAGE / 1024 / Q2_NW;   // row loads per wavefront per stage
 constexpr int Q2_FR = 8;                   // ring of per-group side data
 constexpr int Q2_KMAX = 32;                // largest k
+constexpr int Q2_LDS = 160 * 1024;         // LDS of a CU
 
 // s_waitcnt immediate: at most n vector-memory operations outstanding
 constexpr int q2_vmcnt(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
@@ -98,7 +99,7 @@ struct Q2Pair {
     int i;
 };
 
-template <int DT, int RB, int MQ>
+template <int DT, int RB, int MQ, int KR>
 struct Q2Cfg {
     typedef typename Q2Op<DT>::Step Step;
     static constexpr int UPS = Q2Op<DT>::UPS;         // 16-byte units per MFMA step
@@ -107,7 +108,10 @@ struct Q2Cfg {
     static constexpr int QST = RB / 32 / UPS;         // steps of a query row held by a lane
     static constexpr int BQW = MQ * 32;               // queries per wavefront
     static constexpr int BQ = Q2_NW * BQW;            // queries per workgroup
-    static constexpr int NS = MQ == 1 ? 7 : 5;        // stages in the LDS ring
+    static constexpr int LIST_BYTES = Q2_NW * MQ * KR * 64 * 8;
+    static constexpr int SIDE_BYTES = Q2_FR * (Q2_GR + 4) * 4 + Q2_FR * Q2_NW * BQW * 4;
+    static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / Q2_STAGE;   // stages in the LDS ring
+    static_assert(NS >= 4, "LDS ring too small");
     static_assert(RB % Q2_SB == 0 && SPG >= 2, "rows must be at least two whole stages");
     static_assert(SPG <= 6, "wait_stage covers up to six stages per group");
     static_assert(Q2_STAGE % (1024 * Q2_NW) == 0, "stage loads split evenly over the wavefronts");
@@ -135,7 +139,7 @@ struct Q2Cfg {
         uint8_t e[NS * Q2_STAGE];
         float fe[Q2_FR][Q2_GR + 4];             // entry factors of a group, then {max, min, -, -}
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
-        Q2Pair lst[Q2_NW][Q2_KMAX][BQW];        // per-wavefront lists, slot-major
+        uint64_t lst[Q2_NW][MQ][KR][64];        // per-lane lists of keys, slot-major
     };
 };
 
@@ -150,46 +154,74 @@ __device__ inline void q2_mma(f32x16& c, const typename Q2Op<DT>::Step a, const 
         c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-// worst pair of a list of k (the one every other pair comes before): all
-// KR slots are read at once, slots >= k count as the best possible pair, and
-// a tree of comparisons picks the worst
-template <int KR, int BQW>
-__device__ inline void q2_worst(const Q2Pair (*lst)[BQW], int col, int k, float& ws, int& wi, int& wp)
+// A (score, entry) pair as one 64-bit key ordered like (score desc, entry
+// asc): the high word is the score's bits mapped to an order-preserving
+// unsigned integer, the low word the complement of the entry index.  Key 0
+// marks an empty slot (below every pair).
+__device__ inline uint64_t q2_pack(float s, int e)
 {
-    float xs[KR];
-    int xi[KR], xp[KR];
+    const uint32_t u = __float_as_uint(s);
+    const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)e;
+}
+__device__ inline float q2_key_score(uint64_t key)
+{
+    if (key == 0) return neg_inf();
+    const uint32_t o = (uint32_t)(key >> 32);
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+__device__ inline int q2_key_entry(uint64_t key) { return key == 0 ? IDX_NONE : (int)~(uint32_t)key; }
+
+// smallest key of a lane's list (slots past k hold ~0 and are never the smallest):
+// all KR slots are read at once, then a tree of comparisons
+template <int KR>
+__device__ inline void q2_worst(const uint64_t* col, uint64_t& wkey, int& wp)
+{
+    uint64_t x[KR];
+    int xp[KR];
 #pragma unroll
     for (int p = 0; p < KR; ++p) {
-        const Q2Pair x = lst[p][col];
-        xs[p] = p < k ? x.s : __builtin_huge_valf();
-        xi[p] = p < k ? x.i : -1;
+        x[p] = col[p * 64];
         xp[p] = p;
     }
 #pragma unroll
     for (int w = 1; w < KR; w *= 2)
 #pragma unroll
         for (int p = 0; p + w < KR; p += 2 * w) {
-            const bool tk = before(xs[p], xi[p], xs[p + w], xi[p + w]);   // p + w is the worse
-            xs[p] = tk ? xs[p + w] : xs[p];
-            xi[p] = tk ? xi[p + w] : xi[p];
+            const bool tk = x[p + w] < x[p];
+            x[p] = tk ? x[p + w] : x[p];
             xp[p] = tk ? xp[p + w] : xp[p];
         }
-    ws = xs[0];
-    wi = xi[0];
+    wkey = x[0];
     wp = xp[0];
+}
+
+// the 32 values v[eb][r] of a lane, element b = 16 eb + r, chosen by the bits of b
+__device__ inline float q2_pick(const f32x16 (&v)[2], int b)
+{
+    float l[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) l[i] = (b & 16) ? v[1][i] : v[0][i];
+#pragma unroll
+    for (int w = 8; w >= 1; w >>= 1) {
+        const int bit = w == 8 ? 1 : w == 4 ? 2 : w == 2 ? 4 : 8;
+#pragma unroll
+        for (int i = 0; i < w; ++i) l[i] = (b & bit) ? l[2 * i + 1] : l[2 * i];
+    }
+    return l[0];
 }
 
 // grid: workgroup id -> (split, query tile).  With a grid that is a multiple
 // of 8, consecutive linear indices go to the same XCD (workgroups are dealt
 // round-robin over the 8 XCDs), so the query tiles of a split run side by
 // side on one XCD and share its L2.
-template <int DT, int RB, int MQ>
+template <int DT, int RB, int MQ, int KR>
 __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
     const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
     int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i)
 {
-    typedef Q2Cfg<DT, RB, MQ> C;
+    typedef Q2Cfg<DT, RB, MQ, KR> C;
     typedef typename C::Step Step;
     constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
     __shared__ typename C::Smem sm;
@@ -276,16 +308,23 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         }
         fq[mq] = fq_ws[qg];                          // NaN for rows that cannot be matched
     }
-    Q2Pair(*lst)[BQW] = sm.lst[wave];
-    for (int i = lane; i < Q2_KMAX * BQW; i += 64) lst[i / BQW][i % BQW] = Q2Pair{neg_inf(), IDX_NONE};
-    float Ts[MQ];      // worst pair of the query's list (-inf, none while it has empty slots)
-    int Ti[MQ], Wp[MQ], fill[MQ];
+    // per-lane lists: slots below k start empty (key 0), slots from k on hold
+    // ~0 so that they are never the worst
+    uint64_t* lcol[MQ];
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
-        Ts[mq] = neg_inf();
-        Ti[mq] = IDX_NONE;
-        Wp[mq] = 0;
-        fill[mq] = 0;
+        lcol[mq] = &sm.lst[wave][mq][0][lane];
+#pragma unroll
+        for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
+    }
+    uint64_t wkey[MQ];   // smallest key of the lane's list (0 while it has empty slots)
+    int wp[MQ];          // its slot
+    float ps[MQ];        // the partner lane's k-th score (-inf while its list has empty slots)
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) {
+        wkey[mq] = 0;
+        wp[mq] = 0;
+        ps[mq] = neg_inf();
     }
 
     f32x16 acc[MQ][2];
@@ -343,7 +382,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         const int64_t e0 = (g_begin + gi) * Q2_GR;
         const bool whole = e0 + Q2_GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
-        // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f)
+        // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f).
+        // The filter threshold F is the largest valid lower bound on the query's
+        // k-th best score: the lane's own k-th, its partner lane's, the global one.
         const float* fr = sm.fe[gi % Q2_FR];
         const float fmx = fr[Q2_GR], fmn = fr[Q2_GR + 1];
         float G[MQ], F[MQ];
@@ -358,81 +399,55 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 #pragma unroll
                 for (int r = (eb == 0 ? 1 : 0); r < 16; ++r) am = __builtin_fmaxf(am, acc[mq][eb][r]);
             const float ub = am * (am >= 0.f ? fmx : fmn);
-            F[mq] = __builtin_fmaxf(Ts[mq], G[mq]);
+            F[mq] = __builtin_fmaxf(__builtin_fmaxf(q2_key_score(wkey[mq]), ps[mq]), G[mq]);
             pass[mq] = fq[mq] == fq[mq] && clamp1(ub * fq[mq]) >= F[mq];   // NaN f_q: row not matched
             any_pass |= pass[mq];
         }
         if (__builtin_amdgcn_ballot_w64(any_pass)) {
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
-                // exact products, and the quads whose best score reaches the filter
-                uint32_t qbits = 0;
+                // exact scores of the lane's 32 pairs and the ones reaching the filter
+                uint32_t mask = 0;
                 if (pass[mq]) {
 #pragma unroll
-                    for (int p = 0; p < 8; ++p) {
-                        const int eb = p >> 2, g = p & 3;
-                        const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                        const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
-                        float qm = neg_inf();
+                    for (int eb = 0; eb < 2; ++eb)
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float v = acc[mq][eb][4 * g + i] * fv[i];
-                            acc[mq][eb][4 * g + i] = v;
-                            if (whole || 32 * eb + 8 * g + i < lim64) qm = __builtin_fmaxf(qm, v);
-                        }
-                        qbits |= (uint32_t)(qm > neg_inf() && clamp1(qm * fq[mq]) >= F[mq]) << p;
-                    }
-                }
-                const int col = mq * 32 + r32;
+                        for (int g = 0; g < 4; ++g) {
+                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
 #pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2) {
-                    uint32_t mine = h == h2 ? qbits : 0u;
-                    while (__builtin_amdgcn_ballot_w64(mine != 0)) {
-                        const bool act = mine != 0;
-                        const int p = act ? __builtin_ctz(mine) : 0;
-                        mine &= mine - 1;
-                        // the quad's four products (select over the eight quads)
-                        float x[4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            float v = acc[mq][0][i];
-#pragma unroll
-                            for (int pp = 1; pp < 8; ++pp) v = p == pp ? acc[mq][pp >> 2][4 * (pp & 3) + i] : v;
-                            x[i] = v;
-                        }
-                        const int eb = p >> 2, g = p & 3;
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float s = clamp1(x[i] * fq[mq]);
-                            const int e = (int)(e0 + 32 * eb + 8 * g + 4 * h + i);
-                            const bool ok = act && (whole || 32 * eb + 8 * g + i < lim64) && s >= G[mq] &&
-                                            before(s, e, Ts[mq], Ti[mq]);
-                            if (ok) {
-                                lst[Wp[mq]][col] = Q2Pair{s, e};
-                                if (fill[mq] < k - 1) {
-                                    fill[mq] += 1;
-                                    Wp[mq] = fill[mq];
-                                } else {
-                                    fill[mq] = k;
-                                    if (k <= 16) q2_worst<16>(lst, col, k, Ts[mq], Ti[mq], Wp[mq]);
-                                    else q2_worst<Q2_KMAX>(lst, col, k, Ts[mq], Ti[mq], Wp[mq]);
-                                }
+                            for (int i = 0; i < 4; ++i) {
+                                const int r = 4 * g + i;
+                                const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
+                                acc[mq][eb][r] = sc;
+                                const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
+                                mask |= (uint32_t)ok << (16 * eb + r);
                             }
                         }
-                    }
-                    // the other half of the query continues from this half's list state
-                    const int src = h2 * 32 + r32;
-                    Ts[mq] = __shfl(Ts[mq], src, 64);
-                    Ti[mq] = __shfl(Ti[mq], src, 64);
-                    Wp[mq] = __shfl(Wp[mq], src, 64);
-                    fill[mq] = __shfl(fill[mq], src, 64);
                 }
-                // publish a raised k-th score for the other workgroups
-                if (h == 0 && fill[mq] == k && Ts[mq] > G[mq]) {
-                    const int64_t qg = q0w + col;
-                    q2_atomic_max(gthr + qg, q2_key(Ts[mq]));
+                // every lane inserts into its own list, one pair per pass
+                while (__builtin_amdgcn_ballot_w64(mask != 0)) {
+                    const bool act = mask != 0;
+                    const int bsel = act ? __builtin_ctz(mask) : 0;
+                    mask &= mask - 1;
+                    const float sc = q2_pick(acc[mq], bsel);
+                    const int r = bsel & 15;
+                    const int e = (int)(e0 + 32 * (bsel >> 4) + 8 * (r >> 2) + 4 * h + (r & 3));
+                    const uint64_t key = q2_pack(sc, e);
+                    if (act && key > wkey[mq]) {
+                        lcol[mq][wp[mq] * 64] = key;
+                        q2_worst<KR>(lcol[mq], wkey[mq], wp[mq]);
+                    }
                 }
             }
+        }
+        // partner thresholds for the next group, and the global bound
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) {
+            const float own = q2_key_score(wkey[mq]);
+            ps[mq] = __shfl_xor(own, 32, 64);
+            const float best = __builtin_fmaxf(own, ps[mq]);
+            if (h == 0 && best > G[mq]) q2_atomic_max(gthr + q0w + mq * 32 + r32, q2_key(best));
         }
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq)
@@ -443,35 +458,69 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 
     if (!live) return;
-    // ---- each query's list in rank order as the split's partial list ----
-    // lane half h ranks slots h, h + 2, ...; equal pairs (empty slots) are
-    // ordered by slot so that every rank is written once
-    __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
+    // ---- the split's partial list of each query: sort each lane's list,
+    // merge it with the partner lane's, lane half 0 writes the k best ----
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
-        const int col = mq * 32 + r32;
-        const int64_t qg = q0w + col;
-        const int64_t o = ((int64_t)split * b_pad + qg) * k;
-        for (int p = h; p < k; p += 2) {
-            const Q2Pair x = lst[p][col];
-            int rank = 0;
-            for (int p2 = 0; p2 < k; ++p2) {
-                const Q2Pair y = lst[p2][col];
-                rank += before(y.s, y.i, x.s, x.i) || (y.s == x.s && y.i == x.i && p2 < p);
-            }
-            part_s[o + rank] = x.s;
-            part_i[o + rank] = x.i;
+        uint64_t x[KR];
+#pragma unroll
+        for (int p = 0; p < KR; ++p) x[p] = lcol[mq][p * 64] == ~0ull ? 0ull : lcol[mq][p * 64];
+        // bitonic sort, descending
+#pragma unroll
+        for (int size = 2; size <= KR; size *= 2)
+#pragma unroll
+            for (int stride = size / 2; stride > 0; stride /= 2)
+#pragma unroll
+                for (int i = 0; i < KR; ++i) {
+                    const int j = i ^ stride;
+                    if (j > i) {
+                        const bool desc = (i & size) == 0;
+                        const bool sw = desc ? x[i] < x[j] : x[i] > x[j];
+                        const uint64_t a0 = x[i], a1 = x[j];
+                        x[i] = sw ? a1 : a0;
+                        x[j] = sw ? a0 : a1;
+                    }
+                }
+        // the larger of own[p] and partner[KR - 1 - p] is a bitonic sequence
+        // holding the KR largest of both lists; half-cleaners sort it
+        uint64_t m[KR];
+#pragma unroll
+        for (int p = 0; p < KR; ++p) {
+            const uint64_t o = x[KR - 1 - p];
+            const uint32_t lo = __shfl_xor((uint32_t)o, 32, 64), hi = __shfl_xor((uint32_t)(o >> 32), 32, 64);
+            const uint64_t y = ((uint64_t)hi << 32) | lo;            // partner's (KR - 1 - p)-th
+            m[p] = x[p] > y ? x[p] : y;
+        }
+#pragma unroll
+        for (int stride = KR / 2; stride > 0; stride /= 2)
+#pragma unroll
+            for (int i = 0; i < KR; ++i)
+                if ((i & stride) == 0) {
+                    const bool sw = m[i] < m[i + stride];
+                    const uint64_t a0 = m[i], a1 = m[i + stride];
+                    m[i] = sw ? a1 : a0;
+                    m[i + stride] = sw ? a0 : a1;
+                }
+        const int64_t qg = q0w + mq * 32 + r32;
+        if (h == 0 && qg < b_pad) {
+            const int64_t o = ((int64_t)split * b_pad + qg) * k;
+#pragma unroll
+            for (int p = 0; p < KR; ++p)
+                if (p < k) {
+                    part_s[o + p] = q2_key_score(m[p]);
+                    part_i[o + p] = q2_key_entry(m[p]);
+                }
         }
     }
 }
 
-template <int DT, int RB, int MQ>
+template <int DT, int RB, int MQ, int KR>
 hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
                   int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
-    k_qs<DT, RB, MQ><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
+    k_qs<DT, RB, MQ, KR><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
                                             static_cast<const uint8_t*>(q), fq, gthr, b, k, p.splits,
                                             p.qtiles, p.b_pad, ps, pi);
     return hipGetLastError();
@@ -479,15 +528,39 @@ hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* f
 
 }  // namespace
 
-// shape of the query-stationary kernel for a row size (0 = not built)
-template <int DT>
-constexpr int q2_queries(int64_t row_bytes)
+// shape of the query-stationary kernel: rows of 512, 768, 1024 or 1536 bytes,
+// k <= 32.  Lists of 16 slots for k <= 16 (two query blocks per wavefront
+// except for 1536-byte rows), of 32 slots otherwise (one query block).
+constexpr int q2_mq(int64_t row_bytes, int k) { return k <= 16 && row_bytes != 1536 ? 2 : 1; }
+constexpr bool q2_built(int64_t row_bytes, int k)
 {
-    if constexpr (DT == APC_E4M3)
-        return row_bytes == 1024 || row_bytes == 768 || row_bytes == 512 ? Q2Cfg<DT, 512, 2>::BQ : 0;
-    else
-        return row_bytes == 1536 ? Q2Cfg<DT, 1536, 1>::BQ
-             : row_bytes == 1024 || row_bytes == 768 || row_bytes == 512 ? Q2Cfg<DT, 512, 2>::BQ : 0;
+    return (row_bytes == 512 || row_bytes == 768 || row_bytes == 1024 || row_bytes == 1536) && k >= 1 &&
+           k <= Q2_KMAX;
+}
+constexpr int q2_queries(int64_t row_bytes, int k) { return q2_built(row_bytes, k) ? Q2_NW * 32 * q2_mq(row_bytes, k) : 0; }
+
+template <int DT>
+hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
+                       const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+{
+#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
+    if (k <= 16) {
+        switch (rb) {
+        case 1536: return APC_Q2(1536, 1, 16);
+        case 1024: return APC_Q2(1024, 2, 16);
+        case 768: return APC_Q2(768, 2, 16);
+        case 512: return APC_Q2(512, 2, 16);
+        }
+    } else {
+        switch (rb) {
+        case 1536: return APC_Q2(1536, 1, 32);
+        case 1024: return APC_Q2(1024, 1, 32);
+        case 768: return APC_Q2(768, 1, 32);
+        case 512: return APC_Q2(512, 1, 32);
+        }
+    }
+#undef APC_Q2
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_qs_f16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,

@@ -442,7 +442,7 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     MatchPlan p{};
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
-    const int q2b = qs_queries(dt, rb);
+    const int q2b = qs_queries(dt, rb, k);
     const int qsb = qstat_queries(dt, rb);
     if (q2b > 0 && k <= qs_max_k()) {
         // 16-bit or e4m3 rows: queries in VGPRs, cache rows through LDS, one
