@@ -108,7 +108,8 @@ struct Q2Cfg {
     static constexpr int QST = RB / 32 / UPS;         // steps of a query row held by a lane
     static constexpr int BQW = MQ * 32;               // queries per wavefront
     static constexpr int BQ = Q2_NW * BQW;            // queries per workgroup
-    static constexpr int LIST_BYTES = Q2_NW * MQ * KR * 64 * 8;
+    static constexpr bool LREG = MQ == 1;             // lists in registers (else LDS)
+    static constexpr int LIST_BYTES = LREG ? 0 : Q2_NW * MQ * KR * 64 * 8;
     static constexpr int SIDE_BYTES = Q2_FR * (Q2_GR + 4) * 4 + Q2_FR * Q2_NW * BQW * 4;
     static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / Q2_STAGE;   // stages in the LDS ring
     static_assert(NS >= 4, "LDS ring too small");
@@ -139,7 +140,7 @@ struct Q2Cfg {
         uint8_t e[NS * Q2_STAGE];
         float fe[Q2_FR][Q2_GR + 4];             // entry factors of a group, then {max, min, -, -}
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
-        uint64_t lst[Q2_NW][MQ][KR][64];        // per-lane lists of keys, slot-major
+        uint64_t lst[LREG ? 1 : Q2_NW][MQ][LREG ? 1 : KR][64];   // per-lane lists of keys (LDS form), slot-major
     };
 };
 
@@ -196,19 +197,55 @@ __device__ inline void q2_worst(const uint64_t* col, uint64_t& wkey, int& wp)
     wp = xp[0];
 }
 
-// the 32 values v[eb][r] of a lane, element b = 16 eb + r, chosen by the bits of b
+// register form: store key in slot wp, then find the new smallest key
+template <int KR>
+__device__ inline void q2_worst_reg(uint64_t (&lk)[KR], uint64_t key, uint64_t& wkey, int& wp)
+{
+#pragma unroll
+    for (int p = 0; p < KR; ++p) lk[p] = p == wp ? key : lk[p];
+    uint64_t x[KR];
+    int xp[KR];
+#pragma unroll
+    for (int p = 0; p < KR; ++p) {
+        x[p] = lk[p];
+        xp[p] = p;
+    }
+#pragma unroll
+    for (int w = 1; w < KR; w *= 2)
+#pragma unroll
+        for (int p = 0; p + w < KR; p += 2 * w) {
+            const bool tk = x[p + w] < x[p];
+            x[p] = tk ? x[p + w] : x[p];
+            xp[p] = tk ? xp[p + w] : xp[p];
+        }
+    wkey = x[0];
+    wp = xp[0];
+}
+
+// (m & x) | (~m & y) as one instruction the optimizer cannot restructure
+__device__ inline float q2_bsel(uint32_t m, float x, float y)
+{
+    float r;
+    asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(x), "v"(y));
+    return r;
+}
+
+// the 32 values v[eb][r] of a lane, element b = 16 eb + r, chosen by the bits
+// of b through a tree of bit selects (ordinary selects would be folded into one
+// dynamically indexed read, which goes through scratch memory)
 __device__ inline float q2_pick(const f32x16 (&v)[2], int b)
 {
-    float l[16];
+    const uint32_t m0 = 0u - (uint32_t)(b & 1), m1 = 0u - (uint32_t)((b >> 1) & 1), m2 = 0u - (uint32_t)((b >> 2) & 1);
+    const uint32_t m3 = 0u - (uint32_t)((b >> 3) & 1), m4 = 0u - (uint32_t)((b >> 4) & 1);
+    float l16[16], l8[8], l4[4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) l[i] = (b & 16) ? v[1][i] : v[0][i];
+    for (int i = 0; i < 16; ++i) l16[i] = q2_bsel(m4, v[1][i], v[0][i]);
 #pragma unroll
-    for (int w = 8; w >= 1; w >>= 1) {
-        const int bit = w == 8 ? 1 : w == 4 ? 2 : w == 2 ? 4 : 8;
+    for (int i = 0; i < 8; ++i) l8[i] = q2_bsel(m0, l16[2 * i + 1], l16[2 * i]);
 #pragma unroll
-        for (int i = 0; i < w; ++i) l[i] = (b & bit) ? l[2 * i + 1] : l[2 * i];
-    }
-    return l[0];
+    for (int i = 0; i < 4; ++i) l4[i] = q2_bsel(m1, l8[2 * i + 1], l8[2 * i]);
+    const float l2a = q2_bsel(m2, l4[1], l4[0]), l2b = q2_bsel(m2, l4[3], l4[2]);
+    return q2_bsel(m3, l2b, l2a);
 }
 
 // grid: workgroup id -> (split, query tile).  With a grid that is a multiple
@@ -310,12 +347,19 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
     // per-lane lists: slots below k start empty (key 0), slots from k on hold
     // ~0 so that they are never the worst
+    constexpr bool LREG = C::LREG;
     uint64_t* lcol[MQ];
+    uint64_t lk[LREG ? MQ : 1][KR];
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
-        lcol[mq] = &sm.lst[wave][mq][0][lane];
+        if constexpr (LREG) {
 #pragma unroll
-        for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
+            for (int p = 0; p < KR; ++p) lk[mq][p] = p < k ? 0ull : ~0ull;
+        } else {
+            lcol[mq] = &sm.lst[wave][mq][0][lane];
+#pragma unroll
+            for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
+        }
     }
     uint64_t wkey[MQ];   // smallest key of the lane's list (0 while it has empty slots)
     int wp[MQ];          // its slot
@@ -387,6 +431,56 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         // k-th best score: the lane's own k-th, its partner lane's, the global one.
         const float* fr = sm.fe[gi % Q2_FR];
         const float fmx = fr[Q2_GR], fmn = fr[Q2_GR + 1];
+        if (gi == 0 && k <= 16) {
+            // Seed for the first group (the lists are still empty): the 16 quads of
+            // a lane pair are disjoint, so with m = ceil(k/2), the smaller of one
+            // lane's m-th largest quad maximum and the other's (k-m)-th largest
+            // has k pairs at or above it.  Both pairings are valid; keep the larger.
+#pragma unroll
+            for (int mq = 0; mq < MQ; ++mq) {
+                float qm[8];
+#pragma unroll
+                for (int eb = 0; eb < 2; ++eb)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        float x = neg_inf();
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (whole || 32 * eb + 8 * g + i < lim64)
+                                x = __builtin_fmaxf(x, acc[mq][eb][4 * g + i] * fr[eb * 32 + 8 * g + 4 * h + i]);
+                        qm[4 * eb + g] = x;
+                    }
+                // sort descending (bitonic, 8 values)
+#pragma unroll
+                for (int size = 2; size <= 8; size *= 2)
+#pragma unroll
+                    for (int stride = size / 2; stride > 0; stride /= 2)
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            const int j = i ^ stride;
+                            if (j > i) {
+                                const bool desc = (i & size) == 0;
+                                const float a0 = qm[i], a1 = qm[j];
+                                const bool sw = desc ? a0 < a1 : a0 > a1;
+                                qm[i] = sw ? a1 : a0;
+                                qm[j] = sw ? a0 : a1;
+                            }
+                        }
+                const int m1 = (k + 1) / 2, m2 = k - m1;          // 1 <= m1 <= 8, 0 <= m2 <= 8
+                float a1 = qm[0], a2 = qm[0];
+#pragma unroll
+                for (int p = 1; p < 8; ++p) {
+                    a1 = p == m1 - 1 ? qm[p] : a1;
+                    a2 = p == m2 - 1 ? qm[p] : a2;
+                }
+                if (m2 == 0) a2 = __builtin_huge_valf();
+                const float b1 = __shfl_xor(a1, 32, 64), b2 = __shfl_xor(a2, 32, 64);
+                const float seed = __builtin_fmaxf(__builtin_fminf(a1, b2), __builtin_fminf(b1, a2));
+                // as a score (NaN f_q leaves the seed at -inf through the comparison below)
+                const float ss = clamp1(seed * fq[mq]);
+                if (ss > ps[mq]) ps[mq] = ss;
+            }
+        }
         float G[MQ], F[MQ];
         bool pass[MQ];
         bool any_pass = false;
@@ -406,22 +500,28 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         if (__builtin_amdgcn_ballot_w64(any_pass)) {
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
-                // exact scores of the lane's 32 pairs and the ones reaching the filter
+                // exact scores of the quads whose bound reaches the filter, and the
+                // pairs among them that reach it
                 uint32_t mask = 0;
                 if (pass[mq]) {
 #pragma unroll
                     for (int eb = 0; eb < 2; ++eb)
 #pragma unroll
                         for (int g = 0; g < 4; ++g) {
-                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
+                            const float qa = __builtin_fmaxf(__builtin_fmaxf(acc[mq][eb][4 * g], acc[mq][eb][4 * g + 1]),
+                                                             __builtin_fmaxf(acc[mq][eb][4 * g + 2], acc[mq][eb][4 * g + 3]));
+                            const float qub = qa * (qa >= 0.f ? fmx : fmn);
+                            if (clamp1(qub * fq[mq]) >= F[mq]) {
+                                const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                                const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
 #pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const int r = 4 * g + i;
-                                const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
-                                acc[mq][eb][r] = sc;
-                                const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
-                                mask |= (uint32_t)ok << (16 * eb + r);
+                                for (int i = 0; i < 4; ++i) {
+                                    const int r = 4 * g + i;
+                                    const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
+                                    acc[mq][eb][r] = sc;
+                                    const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
+                                    mask |= (uint32_t)ok << (16 * eb + r);
+                                }
                             }
                         }
                 }
@@ -435,8 +535,12 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                     const int e = (int)(e0 + 32 * (bsel >> 4) + 8 * (r >> 2) + 4 * h + (r & 3));
                     const uint64_t key = q2_pack(sc, e);
                     if (act && key > wkey[mq]) {
-                        lcol[mq][wp[mq] * 64] = key;
-                        q2_worst<KR>(lcol[mq], wkey[mq], wp[mq]);
+                        if constexpr (LREG) {
+                            q2_worst_reg<KR>(lk[mq], key, wkey[mq], wp[mq]);
+                        } else {
+                            lcol[mq][wp[mq] * 64] = key;
+                            q2_worst<KR>(lcol[mq], wkey[mq], wp[mq]);
+                        }
                     }
                 }
             }
@@ -464,7 +568,12 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     for (int mq = 0; mq < MQ; ++mq) {
         uint64_t x[KR];
 #pragma unroll
-        for (int p = 0; p < KR; ++p) x[p] = lcol[mq][p * 64] == ~0ull ? 0ull : lcol[mq][p * 64];
+        for (int p = 0; p < KR; ++p) {
+            uint64_t v;
+            if constexpr (LREG) v = lk[mq][p];
+            else v = lcol[mq][p * 64];
+            x[p] = v == ~0ull ? 0ull : v;
+        }
         // bitonic sort, descending
 #pragma unroll
         for (int size = 2; size <= KR; size *= 2)
