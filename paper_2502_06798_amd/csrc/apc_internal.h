@@ -78,6 +78,8 @@ hipError_t launch_qstat(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
 // between workgroups.  qs_queries gives the queries per workgroup (0: not built).
 int qs_queries(int dt, int64_t row_bytes, int k);
 int qs_max_k();
+// entries per group (the unit a split is made of) of the shape qs_queries describes
+int qs_group_rows(int64_t row_bytes, int k);
 // query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
                         float* fq, int* gthr, hipStream_t s);

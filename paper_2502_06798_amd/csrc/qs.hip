@@ -45,6 +45,8 @@ int qs_queries(int dt, int64_t row_bytes, int k)
 
 int qs_max_k() { return Q2_KMAX; }
 
+int qs_group_rows(int64_t row_bytes, int k) { return q2_rows(row_bytes, k); }
+
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
                         float* fq, int* gthr, hipStream_t s)
 {

@@ -5,29 +5,33 @@
 // (its split).  Each wavefront keeps its MQ x 32 query rows in VGPRs for its
 // whole life, as the B operands of 32x32 MFMAs (lane l supplies query row
 // l % 32; half h = l / 32 supplies bytes [64h, 64h + 64) of every 128-byte
-// chunk of d).  Cache rows stream through an LDS ring in stages of 64 rows x
-// 256 bytes, loaded straight from global memory into LDS (no VGPRs held by
-// loads in flight); a 16-byte unit of a row sits at unit ^ (row % 16), so the
-// A-operand reads (lane = row) are free of bank conflicts.  One barrier per
-// stage makes the stage visible to the four wavefronts, which all use it.
-// The 64 rows of a stage form two 32-row blocks, so each wavefront runs
-// 2 x MQ independent accumulation chains; every score is the sum over all of
-// d in float32, in the same order whatever the split or tile.
+// chunk of d).  Cache rows stream through an LDS ring in stages of EB x 32
+// rows x 256 bytes, loaded straight from global memory into LDS (no VGPRs held
+// by loads in flight); a 16-byte unit of a row sits at unit ^ (row % 16), so
+// the A-operand reads (lane = row) are free of bank conflicts.  One barrier
+// per stage makes the stage visible to the four wavefronts, which all use it.
+// The EB 32-row blocks of a stage give each wavefront EB x MQ independent
+// accumulation chains (EB = 4 with one query block, 2 with two); every score
+// is the sum over all of d in float32, in the same order whatever the split
+// or tile.
 //
-// Top-k, per wavefront (its queries are its own, so no cross-wave sync):
-//  * after a group of 64 entries, each lane scales its 32 products by the
-//    entry factors and takes their maximum; clamp(max * f_q) is exactly the
-//    best score among them (scaling by f_q > 0 and clamping are monotone), so
-//    only lanes whose maximum reaches the filter threshold look further;
-//  * the filter threshold is the larger of the query's own k-th pair (its
-//    list in LDS) and a per-query global bound shared by all workgroups
-//    through atomicMax: a published value is the k-th best score of some
-//    subset of the entries, so k entries score at least that much and any
-//    entry below it cannot be in the top-k (ties are kept);
-//  * passing pairs replace the worst pair of the query's list (first filling
-//    empty slots); the two lanes of a query take turns, lane half 0 first.
-// At the end each query's list is sorted by rank (score desc, index asc) and
-// written as the split's partial list; k_topk_merge merges the splits.
+// Top-k, per wavefront (its queries are its own, so no cross-wave sync).
+// The two lanes of a query see disjoint entries; each keeps its own list of
+// the best pairs it has seen (in registers with one query block, in LDS with
+// two), as order-preserving 64-bit keys:
+//  * after a group of EB x 32 entries, a lane's largest product times the
+//    group's largest entry factor (smallest, if the product is negative),
+//    scaled by f_q and clamped, bounds every score the lane computed in it
+//    (scaling and clamping are monotone), so most lanes stop there;
+//  * the filter threshold is the largest known lower bound on the query's
+//    k-th best score: the lane's own k-th, its partner lane's, and a
+//    per-query bound shared by all workgroups through atomic max (a published
+//    value is the k-th best score of some subset of the entries, so k entries
+//    score at least that much; ties with it are kept);
+//  * quads of four rows whose bound reaches it get exact scores, and the pairs
+//    that reach it replace the worst key of the lane's list, one per pass.
+// At the end each lane sorts its list, merges it with its partner's, and the
+// k best are written as the split's partial list; k_topk_merge merges splits.
 #pragma once
 
 #include <type_traits>
@@ -42,9 +46,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int Q2_NW = 4;                   // wavefronts per workgroup
 constexpr int Q2_NT = Q2_NW * 64;
 constexpr int Q2_SB = 256;                 // bytes of each row per stage
-constexpr int Q2_GR = 64;                  // rows per stage and per group (two 32-row blocks)
-constexpr int Q2_STAGE = Q2_GR * Q2_SB;    // 16 KB
-constexpr int Q2_LPW = Q2_STAGE / 1024 / Q2_NW;   // row loads per wavefront per stage
 constexpr int Q2_FR = 8;                   // ring of per-group side data
 constexpr int Q2_KMAX = 32;                // largest k
 constexpr int Q2_LDS = 160 * 1024;         // LDS of a CU
@@ -99,7 +100,7 @@ struct Q2Pair {
     int i;
 };
 
-template <int DT, int RB, int MQ, int KR>
+template <int DT, int RB, int MQ, int KR, int EB>
 struct Q2Cfg {
     typedef typename Q2Op<DT>::Step Step;
     static constexpr int UPS = Q2Op<DT>::UPS;         // 16-byte units per MFMA step
@@ -108,14 +109,19 @@ struct Q2Cfg {
     static constexpr int QST = RB / 32 / UPS;         // steps of a query row held by a lane
     static constexpr int BQW = MQ * 32;               // queries per wavefront
     static constexpr int BQ = Q2_NW * BQW;            // queries per workgroup
+    static constexpr int GR = EB * 32;                // rows per stage and per group (EB blocks of 32)
+    static constexpr int STAGE = GR * Q2_SB;          // bytes of a stage
+    static constexpr int LPW = STAGE / 1024 / Q2_NW;  // row loads per wavefront per stage
+    static constexpr int FSLOT = GR + 2 * EB;         // factors of a group, then {max, min, -, -} per 64 rows
     static constexpr bool LREG = MQ == 1;             // lists in registers (else LDS)
     static constexpr int LIST_BYTES = LREG ? 0 : Q2_NW * MQ * KR * 64 * 8;
-    static constexpr int SIDE_BYTES = Q2_FR * (Q2_GR + 4) * 4 + Q2_FR * Q2_NW * BQW * 4;
-    static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / Q2_STAGE;   // stages in the LDS ring
+    static constexpr int SIDE_BYTES = Q2_FR * FSLOT * 4 + Q2_FR * Q2_NW * BQW * 4;
+    static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
     static_assert(NS >= 4, "LDS ring too small");
+    static_assert(EB == 2 || EB == 4, "two or four blocks per group");
     static_assert(RB % Q2_SB == 0 && SPG >= 2, "rows must be at least two whole stages");
     static_assert(SPG <= 6, "wait_stage covers up to six stages per group");
-    static_assert(Q2_STAGE % (1024 * Q2_NW) == 0, "stage loads split evenly over the wavefronts");
+    static_assert(STAGE % (1024 * Q2_NW) == 0, "stage loads split evenly over the wavefronts");
     // vector-memory operations a wavefront issues after stage t's row loads and
     // before it waits for stage t (j = t % SPG), in steady state: the side
     // loads (entry factors, global thresholds) of every group start in
@@ -123,7 +129,7 @@ struct Q2Cfg {
     static constexpr int after(int j)
     {
         const int starts = j == 0 ? (NS - 2) / SPG + 1 : (j + NS - 2) / SPG;
-        return (NS - 2) * Q2_LPW + 2 * starts;
+        return (NS - 2) * LPW + 2 * starts;
     }
     __device__ static void wait_stage(int j)
     {
@@ -137,8 +143,8 @@ struct Q2Cfg {
         }
     }
     struct Smem {
-        uint8_t e[NS * Q2_STAGE];
-        float fe[Q2_FR][Q2_GR + 4];             // entry factors of a group, then {max, min, -, -}
+        uint8_t e[NS * STAGE];
+        float fe[Q2_FR][FSLOT];                 // entry factors of a group, then per 64 rows {max, min, -, -}
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
         uint64_t lst[LREG ? 1 : Q2_NW][MQ][LREG ? 1 : KR][64];   // per-lane lists of keys (LDS form), slot-major
     };
@@ -230,16 +236,24 @@ __device__ inline float q2_bsel(uint32_t m, float x, float y)
     return r;
 }
 
-// the 32 values v[eb][r] of a lane, element b = 16 eb + r, chosen by the bits
-// of b through a tree of bit selects (ordinary selects would be folded into one
-// dynamically indexed read, which goes through scratch memory)
-__device__ inline float q2_pick(const f32x16 (&v)[2], int b)
+// the 16 EB values v[eb][r] of a lane, element b = 16 eb + r, chosen by the
+// bits of b through a tree of bit selects (ordinary selects would be folded
+// into one dynamically indexed read, which goes through scratch memory)
+template <int EB>
+__device__ inline float q2_pick(const f32x16 (&v)[EB], int b)
 {
     const uint32_t m0 = 0u - (uint32_t)(b & 1), m1 = 0u - (uint32_t)((b >> 1) & 1), m2 = 0u - (uint32_t)((b >> 2) & 1);
     const uint32_t m3 = 0u - (uint32_t)((b >> 3) & 1), m4 = 0u - (uint32_t)((b >> 4) & 1);
     float l16[16], l8[8], l4[4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) l16[i] = q2_bsel(m4, v[1][i], v[0][i]);
+    for (int i = 0; i < 16; ++i) {
+        if constexpr (EB == 2) {
+            l16[i] = q2_bsel(m4, v[1][i], v[0][i]);
+        } else {
+            const uint32_t m5 = 0u - (uint32_t)((b >> 5) & 1);
+            l16[i] = q2_bsel(m5, q2_bsel(m4, v[3][i], v[2][i]), q2_bsel(m4, v[1][i], v[0][i]));
+        }
+    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) l8[i] = q2_bsel(m0, l16[2 * i + 1], l16[2 * i]);
 #pragma unroll
@@ -252,15 +266,17 @@ __device__ inline float q2_pick(const f32x16 (&v)[2], int b)
 // of 8, consecutive linear indices go to the same XCD (workgroups are dealt
 // round-robin over the 8 XCDs), so the query tiles of a split run side by
 // side on one XCD and share its L2.
-template <int DT, int RB, int MQ, int KR>
+template <int DT, int RB, int MQ, int KR, int EB>
 __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
     const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
     int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i)
 {
-    typedef Q2Cfg<DT, RB, MQ, KR> C;
+    typedef Q2Cfg<DT, RB, MQ, KR, EB> C;
     typedef typename C::Step Step;
     constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
+    constexpr int GR = C::GR, STAGE = C::STAGE, LPW = C::LPW, FSLOT = C::FSLOT;
+    typedef typename std::conditional<EB == 4, uint64_t, uint32_t>::type Mask;   // one bit per value of a lane
     __shared__ typename C::Smem sm;
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -272,49 +288,49 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const int64_t q0w = (int64_t)qtile * C::BQ + wave * BQW;      // this wavefront's first query
     const bool live = q0w < b;                                     // uniform per wavefront
 
-    const int64_t ngr = (n + Q2_GR - 1) / Q2_GR;                   // 64-row groups of the cache
-    const float* fb = fe + factor_pad(n);                          // per-group factor bounds
+    const int64_t ngr = (n + GR - 1) / GR;                         // groups of the cache
+    const float* fb = fe + factor_pad(n);                          // factor bounds per 64 rows
     const int64_t g_begin = ngr * split / splits;
     const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
     const int T = ng * SPG;                                        // stages of this split
 
-    // ---- stage loads: wavefront w fills rows [16w, 16w + 16) of a stage ----
+    // ---- stage loads: wavefront w fills rows [w GR/4, (w + 1) GR/4) of a stage ----
     const uint32_t lds_e = (uint32_t)(size_t)(lds_void*)sm.e;
     const uint32_t lds_fe = (uint32_t)(size_t)(lds_void*)&sm.fe[0][0];
     const uint32_t lds_gt = (uint32_t)(size_t)(lds_void*)&sm.gthr[0][0][0];
-    int lrow[Q2_LPW], loff[Q2_LPW];
+    int lrow[LPW], loff[LPW];
 #pragma unroll
-    for (int i = 0; i < Q2_LPW; ++i) {
-        lrow[i] = wave * (Q2_GR / Q2_NW) + i * 4 + (lane >> 4);
+    for (int i = 0; i < LPW; ++i) {
+        lrow[i] = wave * (GR / Q2_NW) + i * 4 + (lane >> 4);
         loff[i] = ((lane & 15) ^ (lrow[i] & 15)) * 16;             // logical unit stored at unit lane % 16
     }
     // row pointers of the group being issued (groups are issued in order); a
     // stage j of the group adds j * 256 to them (not through the load's offset
     // field: for loads into LDS that offset moves the LDS address too)
-    const uint8_t* rowp[Q2_LPW];
+    const uint8_t* rowp[LPW];
     auto issue = [&](int gi, auto jc) __attribute__((always_inline)) {                            // stage j of group gi
         constexpr int j = decltype(jc)::value;
-        const int64_t e0 = (g_begin + gi) * Q2_GR;
+        const int64_t e0 = (g_begin + gi) * GR;
         if constexpr (j == 0) {
             const int64_t last = n - 1 - e0;                       // last valid row of the group
 #pragma unroll
-            for (int i = 0; i < Q2_LPW; ++i) {
+            for (int i = 0; i < LPW; ++i) {
                 const int64_t row = lrow[i] < last ? lrow[i] : last;
                 rowp[i] = emb + (e0 + row) * RB + loff[i];
             }
         }
         const int t = gi * SPG + j;
-        const uint32_t sbase = lds_e + (uint32_t)(t % NS) * Q2_STAGE;
+        const uint32_t sbase = lds_e + (uint32_t)(t % NS) * STAGE;
 #pragma unroll
-        for (int i = 0; i < Q2_LPW; ++i)
+        for (int i = 0; i < LPW; ++i)
             q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
-                                              sbase + (uint32_t)(wave * (Q2_GR / Q2_NW) + i * 4) * Q2_SB));
+                                              sbase + (uint32_t)(wave * (GR / Q2_NW) + i * 4) * Q2_SB));
         if constexpr (j == 0) {
-            // the group's 64 entry factors (padded to whole groups) with its
-            // factor bounds, and this wavefront's global bounds: one load each,
-            // lanes beyond the data idle
-            const float* fsrc = lane < Q2_GR / 4 ? fe + e0 + lane * 4 : fb + (g_begin + gi) * 4;
-            if (lane <= Q2_GR / 4) q2_dma16(fsrc, lds_fe + (uint32_t)(gi % Q2_FR) * ((Q2_GR + 4) * 4));
+            // the group's GR entry factors (padded to whole groups) with the
+            // factor bounds of its 64-row parts, and this wavefront's global
+            // bounds: one load each, lanes beyond the data idle
+            const float* fsrc = lane < GR / 4 ? fe + e0 + lane * 4 : fb + (e0 / 64 + (lane - GR / 4)) * 4;
+            if (lane < GR / 4 + EB / 2) q2_dma16(fsrc, lds_fe + (uint32_t)(gi % Q2_FR) * (FSLOT * 4));
             const int gl = lane < BQW / 4 ? lane : 0;
             if (lane < BQW / 4)
                 q2_dma16_fresh(gthr + q0w + gl * 4,
@@ -371,11 +387,11 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         ps[mq] = neg_inf();
     }
 
-    f32x16 acc[MQ][2];
+    f32x16 acc[MQ][EB];
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq)
 #pragma unroll
-        for (int eb = 0; eb < 2; ++eb)
+        for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
 
@@ -389,58 +405,72 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             if (t + NS - 1 < T)                                    // into the slot stage t - 1 used
                 issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
             if (!live) return;
-            const uint8_t* sb = sm.e + (t % NS) * Q2_STAGE + r32 * Q2_SB;
-            Step a[2][SST];
+            const uint8_t* sb = sm.e + (t % NS) * STAGE + r32 * Q2_SB;
+            // step ss of the stage: the A fragments of its EB blocks, then their
+            // MFMAs; the schedule below keeps the reads LA steps ahead
+            Step a[SST][EB];
 #pragma unroll
-            for (int eb = 0; eb < 2; ++eb)
+            for (int ss = 0; ss < SST; ++ss) {
+                const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
+                const int lu = cl * 8 + h * 4 + sp;                      // logical 16-byte unit
 #pragma unroll
-                for (int ss = 0; ss < SST; ++ss) {
-                    const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
-                    const int lu = cl * 8 + h * 4 + sp;                  // logical 16-byte unit
+                for (int eb = 0; eb < EB; ++eb) {
                     const uint8_t* rp = sb + eb * 32 * Q2_SB;
                     if constexpr (UPS == 1) {
-                        a[eb][ss] = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
+                        a[ss][eb] = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
                     } else {
                         const uint4 x0 = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
                         const uint4 x1 = *reinterpret_cast<const uint4*>(rp + (((lu + 1) ^ (r32 & 15)) * 16));
-                        a[eb][ss] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
+                        a[ss][eb] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
                                          (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
                     }
                 }
 #pragma unroll
-            for (int ss = 0; ss < SST; ++ss)
+                for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
-                for (int eb = 0; eb < 2; ++eb)
+                    for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[ss][eb], qv[j * SST + ss][mq]);
+            }
+            // reads run LA steps ahead of the MFMAs that use them (paired with
+            // their own MFMAs, every read's latency would be waited out; all
+            // reads first would hold every fragment of the stage in VGPRs)
+            constexpr int LA = SST < 3 ? SST : 2;
+            __builtin_amdgcn_sched_group_barrier(0x100, LA * EB * UPS, 0);
 #pragma unroll
-                    for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[eb][ss], qv[j * SST + ss][mq]);
-            // reads ahead of the MFMAs (otherwise each read is paired with its MFMA
-            // and every read's latency is waited out)
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 * SST * UPS, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * SST * MQ, 0);
+            for (int ss = 0; ss < SST - LA; ++ss) {
+                __builtin_amdgcn_sched_group_barrier(0x008, EB * MQ, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, EB * UPS, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, LA * EB * MQ, 0);
         });
         if (!live) continue;
 
         // ---- epilogue of the group ----
         // lane (h, c) holds for query c the rows 8 g + 4 h + i (g, i < 4) of each
         // block; quad p = 4 eb + g groups its four rows i
-        const int64_t e0 = (g_begin + gi) * Q2_GR;
-        const bool whole = e0 + Q2_GR <= n;
+        const int64_t e0 = (g_begin + gi) * GR;
+        const bool whole = e0 + GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
         // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f).
         // The filter threshold F is the largest valid lower bound on the query's
         // k-th best score: the lane's own k-th, its partner lane's, the global one.
         const float* fr = sm.fe[gi % Q2_FR];
-        const float fmx = fr[Q2_GR], fmn = fr[Q2_GR + 1];
+        float fmx = fr[GR], fmn = fr[GR + 1];
+#pragma unroll
+        for (int j = 1; j < EB / 2; ++j) {
+            fmx = __builtin_fmaxf(fmx, fr[GR + 4 * j]);
+            fmn = __builtin_fminf(fmn, fr[GR + 4 * j + 1]);
+        }
         if (gi == 0 && k <= 16) {
-            // Seed for the first group (the lists are still empty): the 16 quads of
-            // a lane pair are disjoint, so with m = ceil(k/2), the smaller of one
-            // lane's m-th largest quad maximum and the other's (k-m)-th largest
+            // Seed for the first group (the lists are still empty): the 8 EB quads
+            // of a lane pair are disjoint, so with m = ceil(k/2), the smaller of
+            // one lane's m-th largest quad maximum and the other's (k-m)-th largest
             // has k pairs at or above it.  Both pairings are valid; keep the larger.
+            constexpr int NQ = 4 * EB;                             // quads per lane
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
-                float qm[8];
+                float qm[NQ];
 #pragma unroll
-                for (int eb = 0; eb < 2; ++eb)
+                for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         float x = neg_inf();
@@ -450,13 +480,13 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                                 x = __builtin_fmaxf(x, acc[mq][eb][4 * g + i] * fr[eb * 32 + 8 * g + 4 * h + i]);
                         qm[4 * eb + g] = x;
                     }
-                // sort descending (bitonic, 8 values)
+                // sort descending (bitonic)
 #pragma unroll
-                for (int size = 2; size <= 8; size *= 2)
+                for (int size = 2; size <= NQ; size *= 2)
 #pragma unroll
                     for (int stride = size / 2; stride > 0; stride /= 2)
 #pragma unroll
-                        for (int i = 0; i < 8; ++i) {
+                        for (int i = 0; i < NQ; ++i) {
                             const int j = i ^ stride;
                             if (j > i) {
                                 const bool desc = (i & size) == 0;
@@ -469,7 +499,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 const int m1 = (k + 1) / 2, m2 = k - m1;          // 1 <= m1 <= 8, 0 <= m2 <= 8
                 float a1 = qm[0], a2 = qm[0];
 #pragma unroll
-                for (int p = 1; p < 8; ++p) {
+                for (int p = 1; p < NQ; ++p) {
                     a1 = p == m1 - 1 ? qm[p] : a1;
                     a2 = p == m2 - 1 ? qm[p] : a2;
                 }
@@ -489,7 +519,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             G[mq] = q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]);
             float am = acc[mq][0][0];
 #pragma unroll
-            for (int eb = 0; eb < 2; ++eb)
+            for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                 for (int r = (eb == 0 ? 1 : 0); r < 16; ++r) am = __builtin_fmaxf(am, acc[mq][eb][r]);
             const float ub = am * (am >= 0.f ? fmx : fmn);
@@ -502,10 +532,10 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             for (int mq = 0; mq < MQ; ++mq) {
                 // exact scores of the quads whose bound reaches the filter, and the
                 // pairs among them that reach it
-                uint32_t mask = 0;
+                Mask mask = 0;
                 if (pass[mq]) {
 #pragma unroll
-                    for (int eb = 0; eb < 2; ++eb)
+                    for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                         for (int g = 0; g < 4; ++g) {
                             const float qa = __builtin_fmaxf(__builtin_fmaxf(acc[mq][eb][4 * g], acc[mq][eb][4 * g + 1]),
@@ -520,7 +550,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                                     const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
                                     acc[mq][eb][r] = sc;
                                     const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
-                                    mask |= (uint32_t)ok << (16 * eb + r);
+                                    mask |= (Mask)ok << (16 * eb + r);
                                 }
                             }
                         }
@@ -528,9 +558,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 // every lane inserts into its own list, one pair per pass
                 while (__builtin_amdgcn_ballot_w64(mask != 0)) {
                     const bool act = mask != 0;
-                    const int bsel = act ? __builtin_ctz(mask) : 0;
+                    const int bsel = act ? (EB == 4 ? __builtin_ctzll((uint64_t)mask) : __builtin_ctz((uint32_t)mask)) : 0;
                     mask &= mask - 1;
-                    const float sc = q2_pick(acc[mq], bsel);
+                    const float sc = q2_pick<EB>(acc[mq], bsel);
                     const int r = bsel & 15;
                     const int e = (int)(e0 + 32 * (bsel >> 4) + 8 * (r >> 2) + 4 * h + (r & 3));
                     const uint64_t key = q2_pack(sc, e);
@@ -556,7 +586,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq)
 #pragma unroll
-            for (int eb = 0; eb < 2; ++eb)
+            for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
     }
@@ -623,13 +653,13 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 }
 
-template <int DT, int RB, int MQ, int KR>
+template <int DT, int RB, int MQ, int KR, int EB>
 hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
                   int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
-    k_qs<DT, RB, MQ, KR><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
+    k_qs<DT, RB, MQ, KR, EB><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
                                             static_cast<const uint8_t*>(q), fq, gthr, b, k, p.splits,
                                             p.qtiles, p.b_pad, ps, pi);
     return hipGetLastError();
@@ -641,6 +671,13 @@ hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* f
 // k <= 32.  Lists of 16 slots for k <= 16 (two query blocks per wavefront
 // except for 1536-byte rows), of 32 slots otherwise (one query block).
 constexpr int q2_mq(int64_t row_bytes, int k) { return k <= 16 && row_bytes != 1536 ? 2 : 1; }
+// 32-row blocks per stage and group: four with one query block (two where
+// 1536-byte rows and 32-slot lists leave too few registers), two with two
+constexpr int q2_eb(int64_t row_bytes, int k)
+{
+    return q2_mq(row_bytes, k) == 2 || (row_bytes == 1536 && k > 16) ? 2 : 4;
+}
+constexpr int q2_rows(int64_t row_bytes, int k) { return 32 * q2_eb(row_bytes, k); }
 constexpr bool q2_built(int64_t row_bytes, int k)
 {
     return (row_bytes == 512 || row_bytes == 768 || row_bytes == 1024 || row_bytes == 1536) && k >= 1 &&
@@ -652,7 +689,7 @@ template <int DT>
 hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
                        const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
-#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
+#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
     if (k <= 16) {
         switch (rb) {
         case 1536: return APC_Q2(1536, 1, 16);

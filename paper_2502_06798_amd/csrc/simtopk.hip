@@ -451,7 +451,8 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
         p.bq = q2b;
         p.qtiles = (b + p.bq - 1) / p.bq;
         if (p.qtiles < 1) p.qtiles = 1;
-        const int64_t ngr = (n + 63) / 64;
+        const int64_t gr = qs_group_rows(rb, k);
+        const int64_t ngr = (n + gr - 1) / gr;
         int64_t splits = p.qtiles >= 256 ? 1 : 256 / p.qtiles;
         if (splits > ngr) splits = ngr;
         if (splits < 1) splits = 1;
