@@ -6,16 +6,18 @@ namespace apc {
 namespace {
 
 // query factors f = 1/|q| (NaN for rows that cannot be matched: non-finite,
-// zero norm, bad e4m3 scale, or padding) and reset global bounds, one
-// wavefront per padded query row
+// zero norm, bad e4m3 scale, or padding), reset global bounds and (if hist is
+// not null) clear the score histograms, one wavefront per padded query row
 template <int DT>
 __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, const float* __restrict__ q_scale,
                                                 int32_t b, int64_t b_pad, int64_t row_bytes,
-                                                float* __restrict__ fq, int* __restrict__ gthr)
+                                                float* __restrict__ fq, int* __restrict__ gthr,
+                                                uint32_t* __restrict__ hist)
 {
     const int lane = threadIdx.x & 63;
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (r >= b_pad) return;
+    if (hist != nullptr && lane < Q2_HW) hist[r * Q2_HW + lane] = 0u;
     float ss = 0.f;
     bool bad = false;
     if (r < b) {
@@ -48,28 +50,28 @@ int qs_max_k() { return Q2_KMAX; }
 int qs_group_rows(int64_t row_bytes, int k) { return q2_rows(row_bytes, k); }
 
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, hipStream_t s)
+                        float* fq, int* gthr, uint32_t* hist, hipStream_t s)
 {
     const dim3 grid((unsigned)((b_pad + 3) / 4)), block(256);
     const uint8_t* qp = static_cast<const uint8_t*>(q);
     switch (dt) {
-    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    default: k_qprep<APC_F32><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, hist); break;
+    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, hist); break;
+    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, hist); break;
+    default: k_qprep<APC_F32><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, hist); break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
-                     const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
-                     hipStream_t s)
+                     const void* q, const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps,
+                     int* pi, hipStream_t s)
 {
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     switch (dt) {
-    case APC_F16: return launch_qs_f16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-    case APC_BF16: return launch_qs_bf16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-    case APC_E4M3: return launch_qs_e4m3(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_F16: return launch_qs_f16(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
+    case APC_BF16: return launch_qs_bf16(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
+    case APC_E4M3: return launch_qs_e4m3(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -49,6 +49,25 @@ constexpr int Q2_SB = 256;                 // bytes of each row per stage
 constexpr int Q2_FR = 8;                   // ring of per-group side data
 constexpr int Q2_KMAX = 32;                // largest k
 constexpr int Q2_LDS = 160 * 1024;         // LDS of a CU
+constexpr int Q2_HW = 33;                  // words of a query's score histogram: 66 bins of 16-bit counts
+
+// Histogram bins of a score: 0 holds everything below 2^-8, bins 1..64 split
+// [2^-8, 1) into eight octaves of eight equal parts (the exponent and the top
+// three mantissa bits of the float), bin 65 holds 1.  So bin(s) >= j exactly
+// when s >= q2_bin_edge(j), and a count of c scores in bins >= j proves that
+// c pairs score at least that edge.
+__device__ inline int q2_bin(float s)
+{
+    if (!(s >= 0x1p-8f)) return 0;
+    if (s >= 1.0f) return 65;
+    return 1 + (int)((__float_as_uint(s) >> 20) - (119u << 3));
+}
+__device__ inline float q2_bin_edge(int j)
+{
+    if (j <= 0) return -__builtin_huge_valf();
+    if (j >= 65) return 1.0f;
+    return __uint_as_float((uint32_t)(j - 1 + (119 << 3)) << 20);
+}
 
 // s_waitcnt immediate: at most n vector-memory operations outstanding
 constexpr int q2_vmcnt(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
@@ -76,10 +95,14 @@ __device__ inline int q2_key(float f)
 }
 __device__ inline float q2_unkey(int k) { return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff); }
 
-// fire-and-forget atomic max (no return value, nothing to wait for)
+// fire-and-forget atomic max and add (no return value, nothing to wait for)
 __device__ inline void q2_atomic_max(int* p, int v)
 {
     asm volatile("global_atomic_smax %0, %1, off" ::"v"(p), "v"(v) : "memory");
+}
+__device__ inline void q2_atomic_add(uint32_t* p, uint32_t v)
+{
+    asm volatile("global_atomic_add %0, %1, off" ::"v"(p), "v"(v) : "memory");
 }
 
 template <int DT> struct Q2Op { typedef uint4 Step; static constexpr int UPS = 1; };
@@ -100,7 +123,7 @@ struct Q2Pair {
     int i;
 };
 
-template <int DT, int RB, int MQ, int KR, int EB>
+template <int DT, int RB, int MQ, int KR, int EB, bool SMP>
 struct Q2Cfg {
     typedef typename Q2Op<DT>::Step Step;
     static constexpr int UPS = Q2Op<DT>::UPS;         // 16-byte units per MFMA step
@@ -114,9 +137,12 @@ struct Q2Cfg {
     static constexpr int LPW = STAGE / 1024 / Q2_NW;  // row loads per wavefront per stage
     static constexpr int FSLOT = GR + 2 * EB;         // factors of a group, then {max, min, -, -} per 64 rows
     static constexpr bool LREG = MQ == 1;             // lists in registers (else LDS)
-    static constexpr int LIST_BYTES = LREG ? 0 : Q2_NW * MQ * KR * 64 * 8;
+    static constexpr bool LLDS = !LREG && !SMP;       // lists in LDS (a sampling pass keeps none)
+    static constexpr int LIST_BYTES = LLDS ? Q2_NW * MQ * KR * 64 * 8 : 0;
+    static constexpr int HIST_BYTES = SMP ? Q2_NW * BQW * Q2_HW * 4 : 0;
     static constexpr int SIDE_BYTES = Q2_FR * FSLOT * 4 + Q2_FR * Q2_NW * BQW * 4;
-    static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
+    static constexpr int SIDE = SMP ? 1 : 2;          // side loads per group start
+    static constexpr int NS = (Q2_LDS - LIST_BYTES - HIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
     static_assert(NS >= 4, "LDS ring too small");
     static_assert(EB == 2 || EB == 4, "two or four blocks per group");
     static_assert(RB % Q2_SB == 0 && SPG >= 2, "rows must be at least two whole stages");
@@ -129,7 +155,7 @@ struct Q2Cfg {
     static constexpr int after(int j)
     {
         const int starts = j == 0 ? (NS - 2) / SPG + 1 : (j + NS - 2) / SPG;
-        return (NS - 2) * LPW + 2 * starts;
+        return (NS - 2) * LPW + SIDE * starts;
     }
     __device__ static void wait_stage(int j)
     {
@@ -146,7 +172,8 @@ struct Q2Cfg {
         uint8_t e[NS * STAGE];
         float fe[Q2_FR][FSLOT];                 // entry factors of a group, then per 64 rows {max, min, -, -}
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
-        uint64_t lst[LREG ? 1 : Q2_NW][MQ][LREG ? 1 : KR][64];   // per-lane lists of keys (LDS form), slot-major
+        uint64_t lst[LLDS ? Q2_NW : 1][MQ][LLDS ? KR : 1][64];   // per-lane lists of keys (LDS form), slot-major
+        uint32_t hist[SMP ? Q2_NW : 1][SMP ? BQW : 1][Q2_HW];  // score histograms of a sampling pass
     };
 };
 
@@ -266,13 +293,23 @@ __device__ inline float q2_pick(const f32x16 (&v)[EB], int b)
 // of 8, consecutive linear indices go to the same XCD (workgroups are dealt
 // round-robin over the 8 XCDs), so the query tiles of a split run side by
 // side on one XCD and share its L2.
-template <int DT, int RB, int MQ, int KR, int EB>
+//
+// SMP (sampling pass): each workgroup scores one group, group split x gstride
+// of the cache, and adds its queries' score histograms (q2_bin) to hist
+// (b_pad x Q2_HW words, zeroed beforehand); it keeps no lists and writes no
+// partial lists.  The main pass (SMP false) then starts every query's filter
+// at the highest bin edge with at least k sampled scores at or above it, when
+// hist is not null: k pairs reach that edge, so no pair below it can be in the
+// top-k.  Both passes compute a pair's score with the same instructions, so a
+// sampled score and the main pass's score of the same pair are equal.
+template <int DT, int RB, int MQ, int KR, int EB, bool SMP>
 __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
     const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
-    int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i)
+    int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i,
+    int64_t gstride, uint32_t* __restrict__ hist)
 {
-    typedef Q2Cfg<DT, RB, MQ, KR, EB> C;
+    typedef Q2Cfg<DT, RB, MQ, KR, EB, SMP> C;
     typedef typename C::Step Step;
     constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
     constexpr int GR = C::GR, STAGE = C::STAGE, LPW = C::LPW, FSLOT = C::FSLOT;
@@ -288,7 +325,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const int64_t q0w = (int64_t)qtile * C::BQ + wave * BQW;      // this wavefront's first query
     const bool live = q0w < b;                                     // uniform per wavefront
 
-    const int64_t ngr = (n + GR - 1) / GR;                         // groups of the cache
+    const int64_t ngr = SMP ? splits : (n + GR - 1) / GR;          // groups of the cache (sampled)
     const float* fb = fe + factor_pad(n);                          // factor bounds per 64 rows
     const int64_t g_begin = ngr * split / splits;
     const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
@@ -310,7 +347,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* rowp[LPW];
     auto issue = [&](int gi, auto jc) __attribute__((always_inline)) {                            // stage j of group gi
         constexpr int j = decltype(jc)::value;
-        const int64_t e0 = (g_begin + gi) * GR;
+        const int64_t e0 = (g_begin + gi) * gstride * GR;
         if constexpr (j == 0) {
             const int64_t last = n - 1 - e0;                       // last valid row of the group
 #pragma unroll
@@ -332,7 +369,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             const float* fsrc = lane < GR / 4 ? fe + e0 + lane * 4 : fb + (e0 / 64 + (lane - GR / 4)) * 4;
             if (lane < GR / 4 + EB / 2) q2_dma16(fsrc, lds_fe + (uint32_t)(gi % Q2_FR) * (FSLOT * 4));
             const int gl = lane < BQW / 4 ? lane : 0;
-            if (lane < BQW / 4)
+            if (!SMP && lane < BQW / 4)
                 q2_dma16_fresh(gthr + q0w + gl * 4,
                                lds_gt + (uint32_t)(((gi % Q2_FR) * Q2_NW + wave) * BQW * 4));
         }
@@ -371,7 +408,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         if constexpr (LREG) {
 #pragma unroll
             for (int p = 0; p < KR; ++p) lk[mq][p] = p < k ? 0ull : ~0ull;
-        } else {
+        } else if constexpr (C::LLDS) {
             lcol[mq] = &sm.lst[wave][mq][0][lane];
 #pragma unroll
             for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
@@ -385,6 +422,39 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         wkey[mq] = 0;
         wp[mq] = 0;
         ps[mq] = neg_inf();
+    }
+    float sbnd[MQ];      // the sampled bound (-inf without a sampling pass)
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) sbnd[mq] = neg_inf();
+    uint32_t* hl = &sm.hist[SMP ? wave : 0][0][0];
+    if constexpr (SMP) {
+        for (int w = lane; w < BQW * Q2_HW; w += 64) hl[w] = 0;
+    } else if (hist != nullptr) {
+        // lane half 1 holds words 17..32 (bins 34..65), half 0 words 0..16;
+        // walk down from the top bin until k sampled scores are at or above it
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) {
+            const uint32_t* hrow = hist + (q0w + mq * 32 + r32) * Q2_HW + 17 * h;
+            uint32_t wv[17];
+#pragma unroll
+            for (int i = 0; i < 17; ++i) wv[i] = (h == 0 || i < 16) ? hrow[i] : 0u;
+            uint32_t tot = 0;
+#pragma unroll
+            for (int i = 0; i < 17; ++i) tot += (wv[i] & 0xffffu) + (wv[i] >> 16);
+            const uint32_t up = __shfl_xor(tot, 32, 64);
+            uint32_t acc_c = h == 0 ? up : 0u;                     // counts in higher bins
+            int jb = -1;
+#pragma unroll
+            for (int i = 16; i >= 0; --i) {
+                const int bh = 2 * (17 * h + i) + 1;
+                acc_c += wv[i] >> 16;
+                jb = (jb < 0 && acc_c >= (uint32_t)k) ? bh : jb;
+                acc_c += wv[i] & 0xffffu;
+                jb = (jb < 0 && acc_c >= (uint32_t)k) ? bh - 1 : jb;
+            }
+            const int jo = __shfl_xor(jb, 32, 64);
+            sbnd[mq] = q2_bin_edge(jb > jo ? jb : jo);
+        }
     }
 
     f32x16 acc[MQ][EB];
@@ -447,7 +517,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         // ---- epilogue of the group ----
         // lane (h, c) holds for query c the rows 8 g + 4 h + i (g, i < 4) of each
         // block; quad p = 4 eb + g groups its four rows i
-        const int64_t e0 = (g_begin + gi) * GR;
+        const int64_t e0 = (g_begin + gi) * gstride * GR;
         const bool whole = e0 + GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
         // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f).
@@ -459,6 +529,35 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         for (int j = 1; j < EB / 2; ++j) {
             fmx = __builtin_fmaxf(fmx, fr[GR + 4 * j]);
             fmn = __builtin_fminf(fmn, fr[GR + 4 * j + 1]);
+        }
+        if constexpr (SMP) {
+            // every valid score into the query's histogram (both lanes of a
+            // query add to the same row; LDS atomics)
+#pragma unroll
+            for (int mq = 0; mq < MQ; ++mq) {
+                uint32_t* hrow = hl + (mq * 32 + r32) * Q2_HW;
+                if (fq[mq] == fq[mq]) {
+#pragma unroll
+                    for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const float sc = clamp1(acc[mq][eb][4 * g + i] * fv[i] * fq[mq]);
+                                const int bn = q2_bin(sc);
+                                if (whole || 32 * eb + 8 * g + i < lim64)
+                                    atomicAdd(hrow + (bn >> 1), 1u << ((bn & 1) * 16));
+                            }
+                        }
+                }
+#pragma unroll
+                for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
+            }
+            continue;
         }
         if (gi == 0 && k <= 16) {
             // Seed for the first group (the lists are still empty): the 8 EB quads
@@ -516,7 +615,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         bool any_pass = false;
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq) {
-            G[mq] = q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]);
+            G[mq] = __builtin_fmaxf(q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]), sbnd[mq]);
             float am = acc[mq][0][0];
 #pragma unroll
             for (int eb = 0; eb < EB; ++eb)
@@ -592,6 +691,14 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 
     if (!live) return;
+    if constexpr (SMP) {
+        // the workgroup's counts into the global histograms (rows past b count nothing)
+        for (int w = lane; w < BQW * Q2_HW; w += 64) {
+            const uint32_t v = hl[w];
+            if (v != 0) q2_atomic_add(hist + q0w * Q2_HW + w, v);
+        }
+        return;
+    }
     // ---- the split's partial list of each query: sort each lane's list,
     // merge it with the partner lane's, lane half 0 writes the k best ----
 #pragma unroll
@@ -653,15 +760,25 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 }
 
+// the sampling pass (when the plan has one), then the main pass
 template <int DT, int RB, int MQ, int KR, int EB>
 hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
-                  int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                  int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
+    const uint8_t* e8 = static_cast<const uint8_t*>(emb);
+    const uint8_t* q8 = static_cast<const uint8_t*>(q);
+    if (p.sample_groups > 0) {
+        const int work = p.sample_groups * p.qtiles;
+        const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
+        k_qs<DT, RB, MQ, KR, EB, true><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.sample_groups,
+                                                          p.qtiles, p.b_pad, ps, pi, p.sample_stride, hist);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
-    k_qs<DT, RB, MQ, KR, EB><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
-                                            static_cast<const uint8_t*>(q), fq, gthr, b, k, p.splits,
-                                            p.qtiles, p.b_pad, ps, pi);
+    k_qs<DT, RB, MQ, KR, EB, false><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.splits, p.qtiles,
+                                                        p.b_pad, ps, pi, 1, p.sample_groups > 0 ? hist : nullptr);
     return hipGetLastError();
 }
 
@@ -687,9 +804,10 @@ constexpr int q2_queries(int64_t row_bytes, int k) { return q2_built(row_bytes, 
 
 template <int DT>
 hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                       const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                       const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
+                       hipStream_t s)
 {
-#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
+#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s)
     if (k <= 16) {
         switch (rb) {
         case 1536: return APC_Q2(1536, 1, 16);
@@ -710,10 +828,13 @@ hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* em
 }
 
 hipError_t launch_qs_f16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                         const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                         const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
+                         hipStream_t s);
 hipError_t launch_qs_bf16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                          const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
+                          hipStream_t s);
 hipError_t launch_qs_e4m3(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                          const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
+                          hipStream_t s);
 
 }  // namespace apc
