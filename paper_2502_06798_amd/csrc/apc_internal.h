@@ -82,11 +82,11 @@ int qs_queries(int dt, int64_t row_bytes, int k);
 int qs_max_k();
 // entries per group (the unit a split is made of) of the shape qs_queries describes
 int qs_group_rows(int64_t row_bytes, int k);
-// query factors into fq, reset bounds gthr and clear the score histograms
-// hist (b_pad x 33 words; may be null), for b_pad rows (rows >= b get NaN)
+// query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, uint32_t* hist, hipStream_t s);
-// the sampling pass into hist (when p.sample_groups > 0), then the main pass
+                        float* fq, int* gthr, hipStream_t s);
+// the sampling pass (when p.sample_groups > 0: its histograms in hist, then
+// the bounds they give in gthr), then the main pass
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
                      const void* q, const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps,
                      int* pi, hipStream_t s);

@@ -95,14 +95,20 @@ __device__ inline int q2_key(float f)
 }
 __device__ inline float q2_unkey(int k) { return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff); }
 
-// fire-and-forget atomic max and add (no return value, nothing to wait for)
+// fire-and-forget atomic max (no return value, nothing to wait for)
 __device__ inline void q2_atomic_max(int* p, int v)
 {
     asm volatile("global_atomic_smax %0, %1, off" ::"v"(p), "v"(v) : "memory");
 }
-__device__ inline void q2_atomic_add(uint32_t* p, uint32_t v)
+
+// an empty asm statement that reads x from VGPRs (x is 16 or 32 bytes)
+template <class T>
+__device__ inline void q2_use(const T& x)
 {
-    asm volatile("global_atomic_add %0, %1, off" ::"v"(p), "v"(v) : "memory");
+    typedef int v4 __attribute__((ext_vector_type(4)));
+    typedef int v8 __attribute__((ext_vector_type(8)));
+    if constexpr (sizeof(T) == 16) asm volatile("" ::"v"(__builtin_bit_cast(v4, x)));
+    else asm volatile("" ::"v"(__builtin_bit_cast(v8, x)));
 }
 
 template <int DT> struct Q2Op { typedef uint4 Step; static constexpr int UPS = 1; };
@@ -295,13 +301,13 @@ __device__ inline float q2_pick(const f32x16 (&v)[EB], int b)
 // side on one XCD and share its L2.
 //
 // SMP (sampling pass): each workgroup scores one group, group split x gstride
-// of the cache, and adds its queries' score histograms (q2_bin) to hist
-// (b_pad x Q2_HW words, zeroed beforehand); it keeps no lists and writes no
-// partial lists.  The main pass (SMP false) then starts every query's filter
-// at the highest bin edge with at least k sampled scores at or above it, when
-// hist is not null: k pairs reach that edge, so no pair below it can be in the
-// top-k.  Both passes compute a pair's score with the same instructions, so a
-// sampled score and the main pass's score of the same pair are equal.
+// of the cache, and writes its queries' score histograms (q2_bin) to hist,
+// laid out [query][split][Q2_HW]; it keeps no lists and writes no partial
+// lists.  k_sample_bound then gives each query the highest bin edge with at
+// least k sampled scores at or above it, as its global bound: k pairs reach
+// that edge, so no pair below it can be in the top-k.  Both passes compute a
+// pair's score with the same instructions, so a sampled score and the main
+// pass's score of the same pair are equal.
 template <int DT, int RB, int MQ, int KR, int EB, bool SMP>
 __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
@@ -398,6 +404,15 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         }
         fq[mq] = fq_ws[qg];                          // NaN for rows that cannot be matched
     }
+    // The compiler waits for these loads here: every value is used by an empty
+    // asm statement, so the loads cannot sink into the main loop, where the
+    // wait for them (counted without the LDS loads) would drain those as well.
+#pragma unroll
+    for (int s2 = 0; s2 < C::QST; ++s2)
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) q2_use(qv[s2][mq]);
+#pragma unroll
+    for (int mq = 0; mq < MQ; ++mq) asm volatile("" ::"v"(fq[mq]));
     // per-lane lists: slots below k start empty (key 0), slots from k on hold
     // ~0 so that they are never the worst
     constexpr bool LREG = C::LREG;
@@ -423,39 +438,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         wp[mq] = 0;
         ps[mq] = neg_inf();
     }
-    float sbnd[MQ];      // the sampled bound (-inf without a sampling pass)
-#pragma unroll
-    for (int mq = 0; mq < MQ; ++mq) sbnd[mq] = neg_inf();
     uint32_t* hl = &sm.hist[SMP ? wave : 0][0][0];
-    if constexpr (SMP) {
+    if constexpr (SMP)
         for (int w = lane; w < BQW * Q2_HW; w += 64) hl[w] = 0;
-    } else if (hist != nullptr) {
-        // lane half 1 holds words 17..32 (bins 34..65), half 0 words 0..16;
-        // walk down from the top bin until k sampled scores are at or above it
-#pragma unroll
-        for (int mq = 0; mq < MQ; ++mq) {
-            const uint32_t* hrow = hist + (q0w + mq * 32 + r32) * Q2_HW + 17 * h;
-            uint32_t wv[17];
-#pragma unroll
-            for (int i = 0; i < 17; ++i) wv[i] = (h == 0 || i < 16) ? hrow[i] : 0u;
-            uint32_t tot = 0;
-#pragma unroll
-            for (int i = 0; i < 17; ++i) tot += (wv[i] & 0xffffu) + (wv[i] >> 16);
-            const uint32_t up = __shfl_xor(tot, 32, 64);
-            uint32_t acc_c = h == 0 ? up : 0u;                     // counts in higher bins
-            int jb = -1;
-#pragma unroll
-            for (int i = 16; i >= 0; --i) {
-                const int bh = 2 * (17 * h + i) + 1;
-                acc_c += wv[i] >> 16;
-                jb = (jb < 0 && acc_c >= (uint32_t)k) ? bh : jb;
-                acc_c += wv[i] & 0xffffu;
-                jb = (jb < 0 && acc_c >= (uint32_t)k) ? bh - 1 : jb;
-            }
-            const int jo = __shfl_xor(jb, 32, 64);
-            sbnd[mq] = q2_bin_edge(jb > jo ? jb : jo);
-        }
-    }
 
     f32x16 acc[MQ][EB];
 #pragma unroll
@@ -476,11 +461,13 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
             if (!live) return;
             const uint8_t* sb = sm.e + (t % NS) * STAGE + r32 * Q2_SB;
-            // step ss of the stage: the A fragments of its EB blocks, then their
-            // MFMAs; the schedule below keeps the reads LA steps ahead
+            // the A fragments of step ss (all EB blocks) are read LA steps ahead
+            // of the MFMAs that use them; a scheduling barrier after each step
+            // keeps the compiler from regrouping the MFMAs by accumulator, which
+            // would wait out every read's latency and every MFMA's
+            constexpr int LA = SST < 3 ? SST : 2;
             Step a[SST][EB];
-#pragma unroll
-            for (int ss = 0; ss < SST; ++ss) {
+            auto rd = [&](int ss) __attribute__((always_inline)) {
                 const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
                 const int lu = cl * 8 + h * 4 + sp;                      // logical 16-byte unit
 #pragma unroll
@@ -495,22 +482,18 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                                          (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
                     }
                 }
+            };
+#pragma unroll
+            for (int ss = 0; ss < LA; ++ss) rd(ss);
+#pragma unroll
+            for (int ss = 0; ss < SST; ++ss) {
+                if (ss + LA < SST) rd(ss + LA);
 #pragma unroll
                 for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                     for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[ss][eb], qv[j * SST + ss][mq]);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            // reads run LA steps ahead of the MFMAs that use them (paired with
-            // their own MFMAs, every read's latency would be waited out; all
-            // reads first would hold every fragment of the stage in VGPRs)
-            constexpr int LA = SST < 3 ? SST : 2;
-            __builtin_amdgcn_sched_group_barrier(0x100, LA * EB * UPS, 0);
-#pragma unroll
-            for (int ss = 0; ss < SST - LA; ++ss) {
-                __builtin_amdgcn_sched_group_barrier(0x008, EB * MQ, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, EB * UPS, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, LA * EB * MQ, 0);
         });
         if (!live) continue;
 
@@ -615,7 +598,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         bool any_pass = false;
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq) {
-            G[mq] = __builtin_fmaxf(q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]), sbnd[mq]);
+            G[mq] = q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]);
             float am = acc[mq][0][0];
 #pragma unroll
             for (int eb = 0; eb < EB; ++eb)
@@ -692,10 +675,10 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 
     if (!live) return;
     if constexpr (SMP) {
-        // the workgroup's counts into the global histograms (rows past b count nothing)
+        // this split's histograms of the wavefront's queries
         for (int w = lane; w < BQW * Q2_HW; w += 64) {
-            const uint32_t v = hl[w];
-            if (v != 0) q2_atomic_add(hist + q0w * Q2_HW + w, v);
+            const int qi = w / Q2_HW, ww = w - qi * Q2_HW;
+            hist[((q0w + qi) * splits + split) * Q2_HW + ww] = hl[w];
         }
         return;
     }
@@ -760,6 +743,13 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 }
 
+}  // namespace
+
+// per-query bounds from the sampling pass's histograms (in qs.hip)
+hipError_t launch_sample_bound(const uint32_t* hist, int splits, int32_t b, int32_t k, int* gthr, hipStream_t s);
+
+namespace {
+
 // the sampling pass (when the plan has one), then the main pass
 template <int DT, int RB, int MQ, int KR, int EB>
 hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
@@ -772,13 +762,14 @@ hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* f
         const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
         k_qs<DT, RB, MQ, KR, EB, true><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.sample_groups,
                                                           p.qtiles, p.b_pad, ps, pi, p.sample_stride, hist);
-        const hipError_t e = hipGetLastError();
+        hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if ((e = launch_sample_bound(hist, p.sample_groups, b, k, gthr, s)) != hipSuccess) return e;
     }
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
     k_qs<DT, RB, MQ, KR, EB, false><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.splits, p.qtiles,
-                                                        p.b_pad, ps, pi, 1, p.sample_groups > 0 ? hist : nullptr);
+                                                        p.b_pad, ps, pi, 1, nullptr);
     return hipGetLastError();
 }
 

@@ -511,7 +511,7 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     p.off_fq = 0;
     p.off_gt = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
     p.off_h = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
-    p.off_ps = align256(p.off_h + (p.sample_groups > 0 ? sizeof(uint32_t) * 33 * (size_t)p.b_pad : 0));
+    p.off_ps = align256(p.off_h + sizeof(uint32_t) * 33 * (size_t)p.sample_groups * p.b_pad);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
     p.bytes = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
     return p;
@@ -541,7 +541,7 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
         uint32_t* hist = p.sample_groups > 0 ? reinterpret_cast<uint32_t*>(w + p.off_h) : nullptr;
-        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, hist, s)) != hipSuccess) return e;
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, s)) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qs(p, dt, n, d, emb, fe, q, fq, gt, hist, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QSTAT) {
