@@ -7,6 +7,7 @@ from __future__ import annotations
 
 import concurrent.futures
 import os
+import re
 import subprocess
 import sys
 
@@ -15,6 +16,11 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libapc.so")
 BUILD = os.path.join(HERE, "_build")
 SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qstat.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "assign.hip", "gather.hip"]
+
+# Kernels in these sources load into LDS with asm and wait for those loads by
+# counting vector-memory operations themselves; a register spill would add
+# scratch loads to the count, so their code must not use scratch memory.
+COUNTED = ["qstat.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -33,10 +39,26 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _check_no_scratch(src: str) -> None:
+    asm = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
+    cmd = [HIPCC, *FLAGS, "--cuda-device-only", "-S", "-x", "hip", os.path.join(CSRC, src), "-o", asm]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")
+    text = open(asm).read()
+    bad = [(m.group(1), int(m.group(2))) for m in re.finditer(
+        r"\.amdhsa_kernel (\S+)(?:.|\n)*?\.amdhsa_private_segment_fixed_size (\d+)", text) if int(m.group(2)) > 0]
+    if bad:
+        raise RuntimeError(f"{src}: kernels using scratch memory (their LDS-load waits would be wrong): {bad}")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+    with concurrent.futures.ThreadPoolExecutor(max_workers=8) as ex:
+        checks = [ex.submit(_check_no_scratch, src) for src in COUNTED]
         objs = list(ex.map(_compile, SOURCES))
+        for c in checks:
+            c.result()
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=300)

@@ -148,7 +148,7 @@ apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, 
     const int64_t n_pad = apc::factor_pad(n);
     apc::BuildStatus* dst = nullptr;
     apc::BuildStatus hst{};
-    if ((e = hipMalloc(&c->fe, sizeof(float) * apc::factor_floats(n))) != hipSuccess) {
+    if ((e = hipMalloc(&c->fe, sizeof(float) * n_pad)) != hipSuccess) {
         delete c;
         return fail(APC_E_NOMEM, "apc_build_cache: hipMalloc of %lld row factors: %s", (long long)n,
                     hipGetErrorString(e));
@@ -166,7 +166,6 @@ apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, 
     if ((e = hipMemsetAsync(c->fe + n, 0, sizeof(float) * (n_pad - n), s)) != hipSuccess ||
         (e = hipMemcpyAsync(dst, &hst, sizeof hst, hipMemcpyHostToDevice, s)) != hipSuccess ||
         (e = apc::launch_row_factors(dt, n, d, emb, row_scale, slot_of_entry, n_slots, c->fe, dst, s)) != hipSuccess ||
-        (e = apc::launch_group_bounds(c->fe, n, n_pad, c->fe + n_pad, s)) != hipSuccess ||
         (e = hipMemcpyAsync(&hst, dst, sizeof hst, hipMemcpyDeviceToHost, s)) != hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess) {
         cleanup();

@@ -34,12 +34,8 @@ hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, co
                               const int32_t* slot_of_entry, int64_t n_slots, float* f,
                               BuildStatus* st, hipStream_t s);
 
-// factor layout of a cache: n_pad = n rounded up to a multiple of 256 factors
-// (zeros past n), then n_pad / 64 groups of {max, min, 0, 0} over each 64-row
-// group's factors
+// factor layout of a cache: n rounded up to a multiple of 256 factors, zeros past n
 __host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }
-__host__ __device__ inline int64_t factor_floats(int64_t n) { return factor_pad(n) + factor_pad(n) / 16; }
-hipError_t launch_group_bounds(const float* f, int64_t n, int64_t n_pad, float* fb, hipStream_t s);
 
 // ---- similarity + top-k ----------------------------------------------------
 enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QSTAT = 3, KERNEL_QS = 4 };

@@ -141,12 +141,11 @@ struct Q2Cfg {
     static constexpr int GR = EB * 32;                // rows per stage and per group (EB blocks of 32)
     static constexpr int STAGE = GR * Q2_SB;          // bytes of a stage
     static constexpr int LPW = STAGE / 1024 / Q2_NW;  // row loads per wavefront per stage
-    static constexpr int FSLOT = GR + 2 * EB;         // factors of a group, then {max, min, -, -} per 64 rows
-    static constexpr bool LREG = MQ == 1;             // lists in registers (else LDS)
+    static constexpr bool LREG = MQ == 1 || RB < 1024; // lists in registers (else LDS)
     static constexpr bool LLDS = !LREG && !SMP;       // lists in LDS (a sampling pass keeps none)
     static constexpr int LIST_BYTES = LLDS ? Q2_NW * MQ * KR * 64 * 8 : 0;
     static constexpr int HIST_BYTES = SMP ? Q2_NW * BQW * Q2_HW * 4 : 0;
-    static constexpr int SIDE_BYTES = Q2_FR * FSLOT * 4 + Q2_FR * Q2_NW * BQW * 4;
+    static constexpr int SIDE_BYTES = Q2_FR * GR * 4 + Q2_FR * Q2_NW * BQW * 4;
     static constexpr int SIDE = SMP ? 1 : 2;          // side loads per group start
     static constexpr int NS = (Q2_LDS - LIST_BYTES - HIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
     static_assert(NS >= 4, "LDS ring too small");
@@ -176,7 +175,7 @@ struct Q2Cfg {
     }
     struct Smem {
         uint8_t e[NS * STAGE];
-        float fe[Q2_FR][FSLOT];                 // entry factors of a group, then per 64 rows {max, min, -, -}
+        float fe[Q2_FR][GR];                    // entry factors of a group
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
         uint64_t lst[LLDS ? Q2_NW : 1][MQ][LLDS ? KR : 1][64];   // per-lane lists of keys (LDS form), slot-major
         uint32_t hist[SMP ? Q2_NW : 1][SMP ? BQW : 1][Q2_HW];  // score histograms of a sampling pass
@@ -236,29 +235,23 @@ __device__ inline void q2_worst(const uint64_t* col, uint64_t& wkey, int& wp)
     wp = xp[0];
 }
 
-// register form: store key in slot wp, then find the new smallest key
+// register form, kept sorted by key descending: insert key (0 inserts
+// nothing), dropping the smallest; every slot compares once and shifts down
+// when the key goes above the slot before it
 template <int KR>
-__device__ inline void q2_worst_reg(uint64_t (&lk)[KR], uint64_t key, uint64_t& wkey, int& wp)
+__device__ inline void q2_insert_sorted(uint64_t (&lk)[KR], uint64_t key)
 {
+    uint64_t prev = lk[0];
+    bool above_prev = key > prev;
+    lk[0] = above_prev ? key : prev;
 #pragma unroll
-    for (int p = 0; p < KR; ++p) lk[p] = p == wp ? key : lk[p];
-    uint64_t x[KR];
-    int xp[KR];
-#pragma unroll
-    for (int p = 0; p < KR; ++p) {
-        x[p] = lk[p];
-        xp[p] = p;
+    for (int p = 1; p < KR; ++p) {
+        const uint64_t cur = lk[p];
+        const bool above = key > cur;
+        lk[p] = above_prev ? prev : (above ? key : cur);
+        prev = cur;
+        above_prev = above;
     }
-#pragma unroll
-    for (int w = 1; w < KR; w *= 2)
-#pragma unroll
-        for (int p = 0; p + w < KR; p += 2 * w) {
-            const bool tk = x[p + w] < x[p];
-            x[p] = tk ? x[p + w] : x[p];
-            xp[p] = tk ? xp[p + w] : xp[p];
-        }
-    wkey = x[0];
-    wp = xp[0];
 }
 
 // (m & x) | (~m & y) as one instruction the optimizer cannot restructure
@@ -267,6 +260,29 @@ __device__ inline float q2_bsel(uint32_t m, float x, float y)
     float r;
     asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(x), "v"(y));
     return r;
+}
+
+// slot i (the same for the whole wavefront, below KR) of a register list,
+// through a tree of bit selects
+template <int KR>
+__device__ inline uint64_t q2_slot(const uint64_t (&lk)[KR], int i)
+{
+    uint32_t lo[KR], hi[KR];
+#pragma unroll
+    for (int p = 0; p < KR; ++p) {
+        lo[p] = (uint32_t)lk[p];
+        hi[p] = (uint32_t)(lk[p] >> 32);
+    }
+#pragma unroll
+    for (int w = 1; w < KR; w *= 2) {
+        const uint32_t m = 0u - (uint32_t)((i / w) & 1);
+#pragma unroll
+        for (int p = 0; p + w < KR; p += 2 * w) {
+            lo[p] = __float_as_uint(q2_bsel(m, __uint_as_float(lo[p + w]), __uint_as_float(lo[p])));
+            hi[p] = __float_as_uint(q2_bsel(m, __uint_as_float(hi[p + w]), __uint_as_float(hi[p])));
+        }
+    }
+    return ((uint64_t)hi[0] << 32) | lo[0];
 }
 
 // the 16 EB values v[eb][r] of a lane, element b = 16 eb + r, chosen by the
@@ -318,7 +334,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     typedef Q2Cfg<DT, RB, MQ, KR, EB, SMP> C;
     typedef typename C::Step Step;
     constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
-    constexpr int GR = C::GR, STAGE = C::STAGE, LPW = C::LPW, FSLOT = C::FSLOT;
+    constexpr int GR = C::GR, STAGE = C::STAGE, LPW = C::LPW;
     typedef typename std::conditional<EB == 4, uint64_t, uint32_t>::type Mask;   // one bit per value of a lane
     __shared__ typename C::Smem sm;
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r32 = lane & 31;
@@ -332,7 +348,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const bool live = q0w < b;                                     // uniform per wavefront
 
     const int64_t ngr = SMP ? splits : (n + GR - 1) / GR;          // groups of the cache (sampled)
-    const float* fb = fe + factor_pad(n);                          // factor bounds per 64 rows
     const int64_t g_begin = ngr * split / splits;
     const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
     const int T = ng * SPG;                                        // stages of this split
@@ -369,11 +384,10 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
                                               sbase + (uint32_t)(wave * (GR / Q2_NW) + i * 4) * Q2_SB));
         if constexpr (j == 0) {
-            // the group's GR entry factors (padded to whole groups) with the
-            // factor bounds of its 64-row parts, and this wavefront's global
-            // bounds: one load each, lanes beyond the data idle
-            const float* fsrc = lane < GR / 4 ? fe + e0 + lane * 4 : fb + (e0 / 64 + (lane - GR / 4)) * 4;
-            if (lane < GR / 4 + EB / 2) q2_dma16(fsrc, lds_fe + (uint32_t)(gi % Q2_FR) * (FSLOT * 4));
+            // the group's GR entry factors (zero-padded to whole groups) and this
+            // wavefront's global bounds: one load each, lanes beyond the data idle
+            const int fl = lane < GR / 4 ? lane : 0;
+            if (lane < GR / 4) q2_dma16(fe + e0 + fl * 4, lds_fe + (uint32_t)(gi % Q2_FR) * (GR * 4));
             const int gl = lane < BQW / 4 ? lane : 0;
             if (!SMP && lane < BQW / 4)
                 q2_dma16_fresh(gthr + q0w + gl * 4,
@@ -413,8 +427,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         for (int mq = 0; mq < MQ; ++mq) q2_use(qv[s2][mq]);
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) asm volatile("" ::"v"(fq[mq]));
-    // per-lane lists: slots below k start empty (key 0), slots from k on hold
-    // ~0 so that they are never the worst
+    // per-lane lists.  Registers: the KR best keys, sorted descending (key 0:
+    // empty).  LDS: slots below k start empty, slots from k on hold ~0 so that
+    // they are never the worst.
     constexpr bool LREG = C::LREG;
     uint64_t* lcol[MQ];
     uint64_t lk[LREG ? MQ : 1][KR];
@@ -422,15 +437,15 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     for (int mq = 0; mq < MQ; ++mq) {
         if constexpr (LREG) {
 #pragma unroll
-            for (int p = 0; p < KR; ++p) lk[mq][p] = p < k ? 0ull : ~0ull;
+            for (int p = 0; p < KR; ++p) lk[mq][p] = 0ull;
         } else if constexpr (C::LLDS) {
             lcol[mq] = &sm.lst[wave][mq][0][lane];
 #pragma unroll
             for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
         }
     }
-    uint64_t wkey[MQ];   // smallest key of the lane's list (0 while it has empty slots)
-    int wp[MQ];          // its slot
+    uint64_t wkey[MQ];   // the lane's k-th key (0 while it has fewer than k)
+    int wp[MQ];          // its slot (lists in LDS)
     float ps[MQ];        // the partner lane's k-th score (-inf while its list has empty slots)
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
@@ -503,16 +518,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         const int64_t e0 = (g_begin + gi) * gstride * GR;
         const bool whole = e0 + GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
-        // bound filter: acc_r * f_r <= max(acc) * (max f if max(acc) >= 0, else min f).
-        // The filter threshold F is the largest valid lower bound on the query's
-        // k-th best score: the lane's own k-th, its partner lane's, the global one.
-        const float* fr = sm.fe[gi % Q2_FR];
-        float fmx = fr[GR], fmn = fr[GR + 1];
-#pragma unroll
-        for (int j = 1; j < EB / 2; ++j) {
-            fmx = __builtin_fmaxf(fmx, fr[GR + 4 * j]);
-            fmn = __builtin_fminf(fmn, fr[GR + 4 * j + 1]);
-        }
+        const float* fr = sm.fe[gi % Q2_FR];             // the group's entry factors
         if constexpr (SMP) {
             // every valid score into the query's histogram (both lanes of a
             // query add to the same row; LDS atomics)
@@ -593,47 +599,60 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 if (ss > ps[mq]) ps[mq] = ss;
             }
         }
+        // The filter threshold F is the largest valid lower bound on the query's
+        // k-th best score: the lane's own k-th, its partner lane's, the global one.
+        // The lane's best score in the group is computed exactly: its largest
+        // product times entry factor, then times f_q and clamped (both monotone).
+        // Rows past n read the zero padding of the factors, which at most lets
+        // the group through to the exact test below.
+        float m[MQ];
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) m[mq] = neg_inf();
+#pragma unroll
+        for (int eb = 0; eb < EB; ++eb) {
+            float fv[16];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                fv[4 * g] = f4.x;
+                fv[4 * g + 1] = f4.y;
+                fv[4 * g + 2] = f4.z;
+                fv[4 * g + 3] = f4.w;
+            }
+#pragma unroll
+            for (int mq = 0; mq < MQ; ++mq)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) m[mq] = __builtin_fmaxf(m[mq], acc[mq][eb][r] * fv[r]);
+        }
         float G[MQ], F[MQ];
         bool pass[MQ];
         bool any_pass = false;
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq) {
             G[mq] = q2_unkey(sm.gthr[gi % Q2_FR][wave][mq * 32 + r32]);
-            float am = acc[mq][0][0];
-#pragma unroll
-            for (int eb = 0; eb < EB; ++eb)
-#pragma unroll
-                for (int r = (eb == 0 ? 1 : 0); r < 16; ++r) am = __builtin_fmaxf(am, acc[mq][eb][r]);
-            const float ub = am * (am >= 0.f ? fmx : fmn);
             F[mq] = __builtin_fmaxf(__builtin_fmaxf(q2_key_score(wkey[mq]), ps[mq]), G[mq]);
-            pass[mq] = fq[mq] == fq[mq] && clamp1(ub * fq[mq]) >= F[mq];   // NaN f_q: row not matched
+            pass[mq] = fq[mq] == fq[mq] && clamp1(m[mq] * fq[mq]) >= F[mq];   // NaN f_q: row not matched
             any_pass |= pass[mq];
         }
         if (__builtin_amdgcn_ballot_w64(any_pass)) {
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
-                // exact scores of the quads whose bound reaches the filter, and the
-                // pairs among them that reach it
+                // exact scores, and the pairs that reach the filter
                 Mask mask = 0;
                 if (pass[mq]) {
 #pragma unroll
                     for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
                         for (int g = 0; g < 4; ++g) {
-                            const float qa = __builtin_fmaxf(__builtin_fmaxf(acc[mq][eb][4 * g], acc[mq][eb][4 * g + 1]),
-                                                             __builtin_fmaxf(acc[mq][eb][4 * g + 2], acc[mq][eb][4 * g + 3]));
-                            const float qub = qa * (qa >= 0.f ? fmx : fmn);
-                            if (clamp1(qub * fq[mq]) >= F[mq]) {
-                                const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                                const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
+                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
 #pragma unroll
-                                for (int i = 0; i < 4; ++i) {
-                                    const int r = 4 * g + i;
-                                    const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
-                                    acc[mq][eb][r] = sc;
-                                    const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
-                                    mask |= (Mask)ok << (16 * eb + r);
-                                }
+                            for (int i = 0; i < 4; ++i) {
+                                const int r = 4 * g + i;
+                                const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
+                                acc[mq][eb][r] = sc;
+                                const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
+                                mask |= (Mask)ok << (16 * eb + r);
                             }
                         }
                 }
@@ -646,15 +665,14 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                     const int r = bsel & 15;
                     const int e = (int)(e0 + 32 * (bsel >> 4) + 8 * (r >> 2) + 4 * h + (r & 3));
                     const uint64_t key = q2_pack(sc, e);
-                    if (act && key > wkey[mq]) {
-                        if constexpr (LREG) {
-                            q2_worst_reg<KR>(lk[mq], key, wkey[mq], wp[mq]);
-                        } else {
-                            lcol[mq][wp[mq] * 64] = key;
-                            q2_worst<KR>(lcol[mq], wkey[mq], wp[mq]);
-                        }
+                    if constexpr (LREG) {
+                        q2_insert_sorted<KR>(lk[mq], act ? key : 0ull);
+                    } else if (act && key > wkey[mq]) {
+                        lcol[mq][wp[mq] * 64] = key;
+                        q2_worst<KR>(lcol[mq], wkey[mq], wp[mq]);
                     }
                 }
+                if constexpr (LREG) wkey[mq] = q2_slot<KR>(lk[mq], k - 1);
             }
         }
         // partner thresholds for the next group, and the global bound
@@ -694,9 +712,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             else v = lcol[mq][p * 64];
             x[p] = v == ~0ull ? 0ull : v;
         }
-        // bitonic sort, descending
+        // bitonic sort, descending (register lists are sorted already)
 #pragma unroll
-        for (int size = 2; size <= KR; size *= 2)
+        for (int size = 2; size <= (LREG ? 1 : KR); size *= 2)
 #pragma unroll
             for (int stride = size / 2; stride > 0; stride /= 2)
 #pragma unroll

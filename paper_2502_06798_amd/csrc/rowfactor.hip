@@ -99,34 +99,7 @@ __global__ __launch_bounds__(256) void k_row_factors(const uint8_t* __restrict__
     }
 }
 
-// max and min entry factor of each 64-row group (rows below n only), stored as
-// four floats per group: a cheap upper bound on acc * f_e over the group
-__global__ __launch_bounds__(256) void k_group_bounds(const float* __restrict__ f, int64_t n, int64_t ngroups,
-                                                      float4* __restrict__ fb)
-{
-    const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (g >= ngroups) return;
-    float mx = 0.f, mn = 0.f;
-    const int64_t r0 = g * 64;
-    if (r0 < n) {
-        mx = mn = f[r0];
-        const int64_t r1 = r0 + 64 < n ? r0 + 64 : n;
-        for (int64_t r = r0 + 1; r < r1; ++r) {
-            mx = __builtin_fmaxf(mx, f[r]);
-            mn = __builtin_fminf(mn, f[r]);
-        }
-    }
-    fb[g] = make_float4(mx, mn, 0.f, 0.f);
-}
-
 }  // namespace
-
-hipError_t launch_group_bounds(const float* f, int64_t n, int64_t n_pad, float* fb, hipStream_t s)
-{
-    const int64_t ngroups = n_pad / 64;
-    k_group_bounds<<<(unsigned)((ngroups + 255) / 256), 256, 0, s>>>(f, n, ngroups, reinterpret_cast<float4*>(fb));
-    return hipGetLastError();
-}
 
 hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, const float* scale,
                               const int32_t* slot_of_entry, int64_t n_slots, float* f,
