@@ -90,26 +90,35 @@ CASES = [
     ("e4m3", 64, 3000, 768, 32),
     ("e4m3", 200, 1500, 112, 7),
     ("f16", 300, 129, 64, 64),
-    # streaming kernel (b <= 256, rows of whole groups of 4 x 128 bytes, 6 x 128 for e4m3;
-    # float rows, or k > 16, or row sizes the query-stationary kernel is not built for)
+    # streaming kernel: float rows, and 16-bit or e4m3 rows of sizes the
+    # query-stationary kernel is not built for (whole groups of 4 x 128 bytes,
+    # 6 x 128 for e4m3), or k > 32
     ("f32", 16, 5000, 768, 5),
-    ("e4m3", 100, 2050, 768, 10),
-    ("f16", 256, 7777, 768, 10),
-    ("bf16", 3, 17, 256, 17),
-    ("f16", 5, 40, 256, 3),
-    ("e4m3", 7, 33, 768, 33),
     ("f16", 64, 1000, 1536, 12),
-    ("f16", 200, 40000, 256, 3),
-    ("bf16", 100, 3000, 768, 20),
-    # query-stationary kernel (k <= 16; f16/bf16 rows of 512, 1024, 1536 bytes,
-    # e4m3 rows of 512 or 768 bytes)
+    # query-stationary kernel: 16-bit or e4m3 rows of 512, 768, 1024 or 1536
+    # bytes, k <= 32; every shape family (rows, query blocks, 32-row blocks per
+    # group, lists in registers or LDS), with and without the sampling pass
+    ("e4m3", 100, 2050, 768, 10),      # 768 B, two query blocks, sampling pass
+    ("f16", 256, 7777, 768, 10),       # 1536 B, one block, four 32-row blocks
+    ("bf16", 3, 17, 256, 17),          # one group, one split
+    ("f16", 5, 40, 256, 3),
+    ("e4m3", 7, 33, 768, 33),          # k > 32: streaming
+    ("bf16", 100, 3000, 768, 20),      # 1536 B, 32-slot lists, two 32-row blocks
     ("f16", 256, 50000, 768, 10),
     ("bf16", 129, 3001, 768, 16),
     ("e4m3", 300, 9000, 768, 10),
     ("f16", 1, 31, 768, 5),
-    ("f16", 40, 100, 512, 7),
-    ("e4m3", 5, 70000, 512, 16),
+    ("f16", 40, 100, 512, 7),          # 1024 B, lists in LDS
+    ("e4m3", 5, 70000, 512, 16),       # 512 B, two query blocks, sampling pass
     ("bf16", 512, 20000, 256, 8),
+    ("f16", 200, 40000, 256, 3),
+    ("f16", 150, 6000, 256, 12),       # 512 B, two query blocks
+    ("f16", 150, 6000, 256, 24),       # 512 B, one block, 32-slot lists
+    ("bf16", 70, 5000, 384, 16),       # 768 B, two query blocks
+    ("f16", 90, 5000, 512, 9),         # 1024 B, two query blocks, lists in LDS
+    ("e4m3", 90, 5000, 1024, 20),      # 1024 B e4m3, one block, 32-slot lists
+    ("e4m3", 33, 4000, 1536, 11),      # 1536 B e4m3, one block, four 32-row blocks
+    ("bf16", 64, 3000, 768, 29),       # 1536 B, 32-slot lists
 ]
 
 
@@ -139,6 +148,30 @@ def test_match_small(apc, orc, dtype, b, n, d, k):
     apc.apc_match_batch(c, q, qs, k, ts2, ti2, ws)
     torch.cuda.synchronize()
     assert torch.equal(ti, ti2) and torch.equal(ts, ts2)
+    c.close()
+
+
+@pytest.mark.parametrize("dtype,b,n,d,k", [("f16", 2048, 40000, 768, 10), ("e4m3", 1024, 60000, 512, 12)])
+def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
+    """Enough query tiles that each split holds many groups: no sampling pass,
+    lists fill and bounds tighten as the pass goes; a subset of rows is checked."""
+    say(f"match (no sampling pass) {dtype} b={b} n={n} d={d} k={k}")
+    e, es = make_rows(n, d, dtype, 30 + n, clusters=max(1, n // 50))
+    q, qs = make_rows(b, d, dtype, 40 + b, clusters=None)
+    q[: b // 2] = e[torch.arange(b // 2, device="cuda") * 13 % n]
+    if qs is not None:
+        qs[: b // 2] = es[torch.arange(b // 2, device="cuda") * 13 % n]
+    c = apc.apc_build_cache(e, es)
+    ts = torch.empty((b, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((b, k), dtype=torch.int32, device="cuda")
+    apc.apc_match_batch(c, q, qs, k, ts, ti, apc.workspace_tensor(c, b, k))
+    torch.cuda.synchronize()
+    rows = np.arange(0, b, 61)
+    qh, eh = stored_np(q), stored_np(e)
+    qsh, esh = np_or_none(qs), np_or_none(es)
+    rs, ri = orc.topk(dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, k)
+    st = check_topk(orc, dtype, qh, qsh, eh, esh, ts.cpu().numpy(), ti.cpu().numpy(), rs, ri, rows=rows)
+    say("  ", st)
     c.close()
 
 
