@@ -45,9 +45,7 @@ struct MatchPlan {
     int qtiles;        // ceil(b / bq)
     int splits;        // workgroups along the entries per query tile
     int64_t b_pad;     // qtiles * bq
-    int sample_groups;     // groups scored by the sampling pass (0: none), one per split
-    int64_t sample_stride; // the sampling pass scores groups 0, stride, 2 stride, ...
-    size_t off_fq, off_gt, off_h, off_ps, off_pi, bytes;   // workspace layout
+    size_t off_fq, off_gt, off_ps, off_pi, bytes;   // workspace layout
 };
 MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k);
 
@@ -81,11 +79,9 @@ int qs_group_rows(int64_t row_bytes, int k);
 // query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
                         float* fq, int* gthr, hipStream_t s);
-// the sampling pass (when p.sample_groups > 0: its histograms in hist, then
-// the bounds they give in gthr), then the main pass
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
-                     const void* q, const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps,
-                     int* pi, hipStream_t s);
+                     const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
+                     hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

@@ -36,57 +36,7 @@ __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, 
     gthr[r] = q2_key(neg_inf());
 }
 
-// One workgroup per query row below b: sum the sampling pass's per-split
-// histograms, find the highest bin j with at least k sampled scores in bins
-// >= j, and set the query's global bound to that bin's lower edge (k pairs
-// score at least that much).
-__global__ __launch_bounds__(512) void k_sample_bound(const uint32_t* __restrict__ hist, int splits, int32_t k,
-                                                      int* __restrict__ gthr)
-{
-    constexpr int NC = 512 / Q2_HW;                       // 15 threads per word
-    __shared__ uint32_t part[NC][Q2_HW];
-    const int t = threadIdx.x;
-    const int64_t q = blockIdx.x;
-    const uint32_t* hq = hist + q * splits * Q2_HW;
-    if (t < NC * Q2_HW) {
-        // 16-bit counts added as pairs: a bin holds at most splits x 128 < 2^16 scores
-        const int w = t % Q2_HW, c = t / Q2_HW;
-        uint32_t sum = 0;
-#pragma unroll 8
-        for (int sp = c; sp < splits; sp += NC) sum += hq[sp * Q2_HW + w];
-        part[c][w] = sum;
-    }
-    __syncthreads();
-    if (t >= 64) return;
-    uint32_t v = 0;
-    if (t < Q2_HW)
-#pragma unroll
-        for (int c = 0; c < NC; ++c) v += part[c][t];
-    const uint32_t lo = v & 0xffffu, hi = v >> 16;        // bins 2t and 2t + 1
-    uint32_t suf = lo + hi;                               // becomes: scores in bins >= 2t
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t x = __shfl_down(suf, o, 64);
-        if (t + o < 64) suf += x;
-    }
-    int j = -1;
-    if (t < Q2_HW) j = suf - lo >= (uint32_t)k ? 2 * t + 1 : (suf >= (uint32_t)k ? 2 * t : -1);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const int x = __shfl_xor(j, o, 64);
-        j = x > j ? x : j;
-    }
-    if (t == 0 && j > 0) gthr[q] = q2_key(q2_bin_edge(j));   // bin 0's edge is -inf: nothing to raise
-}
-
 }  // namespace
-
-hipError_t launch_sample_bound(const uint32_t* hist, int splits, int32_t b, int32_t k, int* gthr, hipStream_t s)
-{
-    if (b <= 0) return hipSuccess;
-    k_sample_bound<<<(unsigned)b, 512, 0, s>>>(hist, splits, k, gthr);
-    return hipGetLastError();
-}
 
 int qs_queries(int dt, int64_t row_bytes, int k)
 {
@@ -112,14 +62,14 @@ hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, 
 }
 
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
-                     const void* q, const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps,
-                     int* pi, hipStream_t s)
+                     const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
+                     hipStream_t s)
 {
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     switch (dt) {
-    case APC_F16: return launch_qs_f16(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
-    case APC_BF16: return launch_qs_bf16(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
-    case APC_E4M3: return launch_qs_e4m3(p, n, rb, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s);
+    case APC_F16: return launch_qs_f16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_BF16: return launch_qs_bf16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_E4M3: return launch_qs_e4m3(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -17,21 +17,22 @@
 //
 // Top-k, per wavefront (its queries are its own, so no cross-wave sync).
 // The two lanes of a query see disjoint entries; each keeps its own list of
-// the best pairs it has seen (in registers with one query block, in LDS with
-// two), as order-preserving 64-bit keys:
-//  * after a group of EB x 32 entries, a lane's largest product times the
-//    group's largest entry factor (smallest, if the product is negative),
-//    scaled by f_q and clamped, bounds every score the lane computed in it
-//    (scaling and clamping are monotone), so most lanes stop there;
+// the best pairs it has seen, as order-preserving 64-bit keys: in registers,
+// sorted, holding the KR best (LDS lists, unsorted, for 1024-byte rows with
+// two query blocks).  After each group of EB x 32 entries:
+//  * a lane's best score in the group is computed exactly (largest product
+//    times entry factor, times f_q, clamped: both steps are monotone), and
+//    only if it reaches the filter threshold does the lane look further;
 //  * the filter threshold is the largest known lower bound on the query's
 //    k-th best score: the lane's own k-th, its partner lane's, and a
 //    per-query bound shared by all workgroups through atomic max (a published
 //    value is the k-th best score of some subset of the entries, so k entries
-//    score at least that much; ties with it are kept);
-//  * quads of four rows whose bound reaches it get exact scores, and the pairs
-//    that reach it replace the worst key of the lane's list, one per pass.
-// At the end each lane sorts its list, merges it with its partner's, and the
-// k best are written as the split's partial list; k_topk_merge merges splits.
+//    score at least that much; ties with it are kept).  The shared bound is
+//    read as late as the LDS ring allows (with the next group's first stage),
+//    so that it includes what other workgroups found meanwhile;
+//  * the pairs that reach it go into the lane's list, one per pass.
+// At the end each lane's list is merged with its partner's, and the k best
+// are written as the split's partial list; k_topk_merge merges the splits.
 #pragma once
 
 #include <type_traits>
@@ -49,26 +50,6 @@ constexpr int Q2_SB = 256;                 // bytes of each row per stage
 constexpr int Q2_FR = 8;                   // ring of per-group side data
 constexpr int Q2_KMAX = 32;                // largest k
 constexpr int Q2_LDS = 160 * 1024;         // LDS of a CU
-constexpr int Q2_HW = 33;                  // words of a query's score histogram: 66 bins of 16-bit counts
-
-// Histogram bins of a score: 0 holds everything below 2^-8, bins 1..64 split
-// [2^-8, 1) into eight octaves of eight equal parts (the exponent and the top
-// three mantissa bits of the float), bin 65 holds 1.  So bin(s) >= j exactly
-// when s >= q2_bin_edge(j), and a count of c scores in bins >= j proves that
-// c pairs score at least that edge.
-__device__ inline int q2_bin(float s)
-{
-    if (!(s >= 0x1p-8f)) return 0;
-    if (s >= 1.0f) return 65;
-    return 1 + (int)((__float_as_uint(s) >> 20) - (119u << 3));
-}
-__device__ inline float q2_bin_edge(int j)
-{
-    if (j <= 0) return -__builtin_huge_valf();
-    if (j >= 65) return 1.0f;
-    return __uint_as_float((uint32_t)(j - 1 + (119 << 3)) << 20);
-}
-
 // s_waitcnt immediate: at most n vector-memory operations outstanding
 constexpr int q2_vmcnt(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
 
@@ -129,7 +110,7 @@ struct Q2Pair {
     int i;
 };
 
-template <int DT, int RB, int MQ, int KR, int EB, bool SMP>
+template <int DT, int RB, int MQ, int KR, int EB>
 struct Q2Cfg {
     typedef typename Q2Op<DT>::Step Step;
     static constexpr int UPS = Q2Op<DT>::UPS;         // 16-byte units per MFMA step
@@ -142,43 +123,44 @@ struct Q2Cfg {
     static constexpr int STAGE = GR * Q2_SB;          // bytes of a stage
     static constexpr int LPW = STAGE / 1024 / Q2_NW;  // row loads per wavefront per stage
     static constexpr bool LREG = MQ == 1 || RB < 1024; // lists in registers (else LDS)
-    static constexpr bool LLDS = !LREG && !SMP;       // lists in LDS (a sampling pass keeps none)
+    static constexpr bool LLDS = !LREG;               // lists in LDS
     static constexpr int LIST_BYTES = LLDS ? Q2_NW * MQ * KR * 64 * 8 : 0;
-    static constexpr int HIST_BYTES = SMP ? Q2_NW * BQW * Q2_HW * 4 : 0;
     static constexpr int SIDE_BYTES = Q2_FR * GR * 4 + Q2_FR * Q2_NW * BQW * 4;
-    static constexpr int SIDE = SMP ? 1 : 2;          // side loads per group start
-    static constexpr int NS = (Q2_LDS - LIST_BYTES - HIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
+    static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / STAGE;   // stages in the LDS ring
     static_assert(NS >= 4, "LDS ring too small");
     static_assert(EB == 2 || EB == 4, "two or four blocks per group");
     static_assert(RB % Q2_SB == 0 && SPG >= 2, "rows must be at least two whole stages");
-    static_assert(SPG <= 6, "wait_stage covers up to six stages per group");
     static_assert(STAGE % (1024 * Q2_NW) == 0, "stage loads split evenly over the wavefronts");
-    // vector-memory operations a wavefront issues after stage t's row loads and
-    // before it waits for stage t (j = t % SPG), in steady state: the side
-    // loads (entry factors, global thresholds) of every group start in
-    // [t, t + NS - 2], and the row loads of stages t + 1 .. t + NS - 2
+    // stages s = t + d, d in [d0, d1], with s % SPG == r, for t % SPG == j
+    static constexpr int count_at(int j, int d0, int d1, int r)
+    {
+        int c = 0;
+        for (int d = d0; d <= d1; ++d) c += ((j + d) % SPG + SPG) % SPG == r;
+        return c;
+    }
+    // Loads of a group's first stage s: the previous group's global bounds (for
+    // its epilogue, read as late as the ring allows), then the rows, then the
+    // group's entry factors.  Vector-memory operations a wavefront issues after
+    // stage t's row loads and before it waits for stage t (j = t % SPG): the
+    // rows of stages t + 1 .. t + NS - 2, entry factors for first stages s in
+    // [t, t + NS - 2], bounds for first stages s in [t + 1, t + NS - 2].
     static constexpr int after(int j)
     {
-        const int starts = j == 0 ? (NS - 2) / SPG + 1 : (j + NS - 2) / SPG;
-        return (NS - 2) * LPW + SIDE * starts;
+        return (NS - 2) * LPW + count_at(j, 0, NS - 2, 0) + count_at(j, 1, NS - 2, 0);
     }
-    __device__ static void wait_stage(int j)
+    // at a group's epilogue, the operations issued after its global bounds: the
+    // loads of the next NS - 1 stages (starting with the next group's first)
+    static constexpr int after_bounds()
     {
-        switch (j) {
-        case 0: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(0))); break;
-        case 1: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(1))); break;
-        case 2: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(2))); break;
-        case 3: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(3))); break;
-        case 4: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(4))); break;
-        default: __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(5))); break;
-        }
+        return (NS - 1) * LPW + count_at(0, 0, NS - 2, 0) + count_at(0, 1, NS - 2, 0);
     }
+    template <int J>
+    __device__ static void wait_stage() { __builtin_amdgcn_s_waitcnt(q2_vmcnt(after(J))); }
     struct Smem {
         uint8_t e[NS * STAGE];
         float fe[Q2_FR][GR];                    // entry factors of a group
         int gthr[Q2_FR][Q2_NW][BQW];            // global bounds (keys) seen at a group start
         uint64_t lst[LLDS ? Q2_NW : 1][MQ][LLDS ? KR : 1][64];   // per-lane lists of keys (LDS form), slot-major
-        uint32_t hist[SMP ? Q2_NW : 1][SMP ? BQW : 1][Q2_HW];  // score histograms of a sampling pass
     };
 };
 
@@ -315,23 +297,13 @@ __device__ inline float q2_pick(const f32x16 (&v)[EB], int b)
 // of 8, consecutive linear indices go to the same XCD (workgroups are dealt
 // round-robin over the 8 XCDs), so the query tiles of a split run side by
 // side on one XCD and share its L2.
-//
-// SMP (sampling pass): each workgroup scores one group, group split x gstride
-// of the cache, and writes its queries' score histograms (q2_bin) to hist,
-// laid out [query][split][Q2_HW]; it keeps no lists and writes no partial
-// lists.  k_sample_bound then gives each query the highest bin edge with at
-// least k sampled scores at or above it, as its global bound: k pairs reach
-// that edge, so no pair below it can be in the top-k.  Both passes compute a
-// pair's score with the same instructions, so a sampled score and the main
-// pass's score of the same pair are equal.
-template <int DT, int RB, int MQ, int KR, int EB, bool SMP>
+template <int DT, int RB, int MQ, int KR, int EB>
 __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
     const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
-    int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i,
-    int64_t gstride, uint32_t* __restrict__ hist)
+    int32_t k, int splits, int qtiles, int64_t b_pad, float* __restrict__ part_s, int* __restrict__ part_i)
 {
-    typedef Q2Cfg<DT, RB, MQ, KR, EB, SMP> C;
+    typedef Q2Cfg<DT, RB, MQ, KR, EB> C;
     typedef typename C::Step Step;
     constexpr int NS = C::NS, SPG = C::SPG, SST = C::SST, UPS = C::UPS, BQW = C::BQW;
     constexpr int GR = C::GR, STAGE = C::STAGE, LPW = C::LPW;
@@ -347,7 +319,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const int64_t q0w = (int64_t)qtile * C::BQ + wave * BQW;      // this wavefront's first query
     const bool live = q0w < b;                                     // uniform per wavefront
 
-    const int64_t ngr = SMP ? splits : (n + GR - 1) / GR;          // groups of the cache (sampled)
+    const int64_t ngr = (n + GR - 1) / GR;                         // groups of the cache
     const int64_t g_begin = ngr * split / splits;
     const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
     const int T = ng * SPG;                                        // stages of this split
@@ -368,7 +340,18 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     const uint8_t* rowp[LPW];
     auto issue = [&](int gi, auto jc) __attribute__((always_inline)) {                            // stage j of group gi
         constexpr int j = decltype(jc)::value;
-        const int64_t e0 = (g_begin + gi) * gstride * GR;
+        if constexpr (j == 0) {
+            if (gi >= 1) {
+                // the previous group's global bounds, for its epilogue: this
+                // wavefront's queries, one load, lanes beyond the data idle
+                const int gl = lane < BQW / 4 ? lane : 0;
+                if (lane < BQW / 4)
+                    q2_dma16_fresh(gthr + q0w + gl * 4,
+                                   lds_gt + (uint32_t)((((gi - 1) % Q2_FR) * Q2_NW + wave) * BQW * 4));
+            }
+            if (gi * SPG >= T) return;                             // past the last stage: bounds only
+        }
+        const int64_t e0 = (g_begin + gi) * GR;
         if constexpr (j == 0) {
             const int64_t last = n - 1 - e0;                       // last valid row of the group
 #pragma unroll
@@ -384,14 +367,10 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
                                               sbase + (uint32_t)(wave * (GR / Q2_NW) + i * 4) * Q2_SB));
         if constexpr (j == 0) {
-            // the group's GR entry factors (zero-padded to whole groups) and this
-            // wavefront's global bounds: one load each, lanes beyond the data idle
+            // the group's GR entry factors (zero-padded to whole groups): one load,
+            // lanes beyond the data idle
             const int fl = lane < GR / 4 ? lane : 0;
             if (lane < GR / 4) q2_dma16(fe + e0 + fl * 4, lds_fe + (uint32_t)(gi % Q2_FR) * (GR * 4));
-            const int gl = lane < BQW / 4 ? lane : 0;
-            if (!SMP && lane < BQW / 4)
-                q2_dma16_fresh(gthr + q0w + gl * 4,
-                               lds_gt + (uint32_t)(((gi % Q2_FR) * Q2_NW + wave) * BQW * 4));
         }
     };
     // stage s = t0 + d of the schedule, with t0 = gi0 * SPG + j0 (j0, d compile-time)
@@ -401,7 +380,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         issue(gi0 + dg, std::integral_constant<int, js>{});
     };
     static_for<NS - 1>([&](auto sc) __attribute__((always_inline)) {
-        if (decltype(sc)::value < T) issue_ahead(0, std::integral_constant<int, 0>{}, sc);
+        if (decltype(sc)::value <= T) issue_ahead(0, std::integral_constant<int, 0>{}, sc);
     });
 
     // ---- queries into VGPRs, factors, empty lists ----
@@ -438,7 +417,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         if constexpr (LREG) {
 #pragma unroll
             for (int p = 0; p < KR; ++p) lk[mq][p] = 0ull;
-        } else if constexpr (C::LLDS) {
+        } else {
             lcol[mq] = &sm.lst[wave][mq][0][lane];
 #pragma unroll
             for (int p = 0; p < KR; ++p) lcol[mq][p * 64] = p < k ? 0ull : ~0ull;
@@ -453,9 +432,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         wp[mq] = 0;
         ps[mq] = neg_inf();
     }
-    uint32_t* hl = &sm.hist[SMP ? wave : 0][0][0];
-    if constexpr (SMP)
-        for (int w = lane; w < BQW * Q2_HW; w += 64) hl[w] = 0;
 
     f32x16 acc[MQ][EB];
 #pragma unroll
@@ -465,16 +441,14 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
 
-    for (int gi = 0; gi < ng; ++gi) {
+    // the stages of logical group gi (every wavefront, for the loads and barriers)
+    auto run_group = [&](int gi) __attribute__((always_inline)) {
         static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
             constexpr int j = decltype(jc)::value;
             const int t = gi * SPG + j;
-            if (t + NS - 2 < T) C::wait_stage(j);
+            if (t + NS - 2 < T) C::template wait_stage<j>();
             else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
             __syncthreads();
-            if (t + NS - 1 < T)                                    // into the slot stage t - 1 used
-                issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
-            if (!live) return;
             const uint8_t* sb = sm.e + (t % NS) * STAGE + r32 * Q2_SB;
             // the A fragments of step ss (all EB blocks) are read LA steps ahead
             // of the MFMAs that use them; a scheduling barrier after each step
@@ -498,8 +472,15 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                     }
                 }
             };
+            // the first reads go out before the stage loads are issued
+            if (live) {
 #pragma unroll
-            for (int ss = 0; ss < LA; ++ss) rd(ss);
+                for (int ss = 0; ss < LA; ++ss) rd(ss);
+            }
+            if (t + NS - 1 <= T)                                   // into the slot stage t - 1 used
+                issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
+            if (!live) return;
+
 #pragma unroll
             for (int ss = 0; ss < SST; ++ss) {
                 if (ss + LA < SST) rd(ss + LA);
@@ -510,44 +491,21 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 __builtin_amdgcn_sched_barrier(0);
             }
         });
+    };
+    for (int gi = 0; gi < ng; ++gi) {
+        run_group(gi);
         if (!live) continue;
+        // the group's global bounds (loaded with the next group's first stage)
+        if ((gi + 1) * SPG + NS - 2 < T) __builtin_amdgcn_s_waitcnt(q2_vmcnt(C::after_bounds()));
+        else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
 
         // ---- epilogue of the group ----
         // lane (h, c) holds for query c the rows 8 g + 4 h + i (g, i < 4) of each
         // block; quad p = 4 eb + g groups its four rows i
-        const int64_t e0 = (g_begin + gi) * gstride * GR;
+        const int64_t e0 = (g_begin + gi) * GR;
         const bool whole = e0 + GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
         const float* fr = sm.fe[gi % Q2_FR];             // the group's entry factors
-        if constexpr (SMP) {
-            // every valid score into the query's histogram (both lanes of a
-            // query add to the same row; LDS atomics)
-#pragma unroll
-            for (int mq = 0; mq < MQ; ++mq) {
-                uint32_t* hrow = hl + (mq * 32 + r32) * Q2_HW;
-                if (fq[mq] == fq[mq]) {
-#pragma unroll
-                    for (int eb = 0; eb < EB; ++eb)
-#pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const float sc = clamp1(acc[mq][eb][4 * g + i] * fv[i] * fq[mq]);
-                                const int bn = q2_bin(sc);
-                                if (whole || 32 * eb + 8 * g + i < lim64)
-                                    atomicAdd(hrow + (bn >> 1), 1u << ((bn & 1) * 16));
-                            }
-                        }
-                }
-#pragma unroll
-                for (int eb = 0; eb < EB; ++eb)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
-            }
-            continue;
-        }
         if (gi == 0 && k <= 16) {
             // Seed for the first group (the lists are still empty): the 8 EB quads
             // of a lane pair are disjoint, so with m = ceil(k/2), the smaller of
@@ -692,14 +650,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 
     if (!live) return;
-    if constexpr (SMP) {
-        // this split's histograms of the wavefront's queries
-        for (int w = lane; w < BQW * Q2_HW; w += 64) {
-            const int qi = w / Q2_HW, ww = w - qi * Q2_HW;
-            hist[((q0w + qi) * splits + split) * Q2_HW + ww] = hl[w];
-        }
-        return;
-    }
     // ---- the split's partial list of each query: sort each lane's list,
     // merge it with the partner lane's, lane half 0 writes the k best ----
 #pragma unroll
@@ -761,33 +711,15 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
 }
 
-}  // namespace
-
-// per-query bounds from the sampling pass's histograms (in qs.hip)
-hipError_t launch_sample_bound(const uint32_t* hist, int splits, int32_t b, int32_t k, int* gthr, hipStream_t s);
-
-namespace {
-
-// the sampling pass (when the plan has one), then the main pass
 template <int DT, int RB, int MQ, int KR, int EB>
 hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
-                  int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                  int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
-    const uint8_t* e8 = static_cast<const uint8_t*>(emb);
-    const uint8_t* q8 = static_cast<const uint8_t*>(q);
-    if (p.sample_groups > 0) {
-        const int work = p.sample_groups * p.qtiles;
-        const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
-        k_qs<DT, RB, MQ, KR, EB, true><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.sample_groups,
-                                                          p.qtiles, p.b_pad, ps, pi, p.sample_stride, hist);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        if ((e = launch_sample_bound(hist, p.sample_groups, b, k, gthr, s)) != hipSuccess) return e;
-    }
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
-    k_qs<DT, RB, MQ, KR, EB, false><<<grid, Q2_NT, 0, s>>>(e8, fe, n, q8, fq, gthr, b, k, p.splits, p.qtiles,
-                                                        p.b_pad, ps, pi, 1, nullptr);
+    k_qs<DT, RB, MQ, KR, EB><<<grid, Q2_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n,
+                                                   static_cast<const uint8_t*>(q), fq, gthr, b, k, p.splits,
+                                                   p.qtiles, p.b_pad, ps, pi);
     return hipGetLastError();
 }
 
@@ -813,10 +745,9 @@ constexpr int q2_queries(int64_t row_bytes, int k) { return q2_built(row_bytes, 
 
 template <int DT>
 hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                       const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
-                       hipStream_t s)
+                       const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
-#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, hist, b, k, ps, pi, s)
+#define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
     if (k <= 16) {
         switch (rb) {
         case 1536: return APC_Q2(1536, 1, 16);
@@ -837,13 +768,10 @@ hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* em
 }
 
 hipError_t launch_qs_f16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                         const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
-                         hipStream_t s);
+                         const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 hipError_t launch_qs_bf16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                          const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
-                          hipStream_t s);
+                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 hipError_t launch_qs_e4m3(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                          const float* fq, int* gthr, uint32_t* hist, int32_t b, int32_t k, float* ps, int* pi,
-                          hipStream_t s);
+                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 
 }  // namespace apc

@@ -457,17 +457,6 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
         if (splits > ngr) splits = ngr;
         if (splits < 1) splits = 1;
         p.splits = (int)splits;
-        // Few groups per split leave the lists shallow for most of the pass, and
-        // most scores then pass the filter.  A sampling pass over one group per
-        // workgroup first gives each query a bound from up to 256 / qtiles
-        // groups spread over the cache (at most 256 groups, so that the 16-bit
-        // histogram counts of 128-row groups cannot overflow).
-        int64_t sg = p.qtiles >= 256 ? 1 : 256 / p.qtiles;
-        if (sg > ngr) sg = ngr;
-        if (ngr / splits <= 16 && sg >= 8) {
-            p.sample_groups = (int)sg;
-            p.sample_stride = ngr / sg;
-        }
     } else if (qsb > 0 && k <= 16 && b <= 2 * qsb) {
         // small batch, 16-bit or e4m3 rows: queries in registers, each cache row
         // staged through LDS once per workgroup
@@ -510,8 +499,7 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     p.b_pad = (int64_t)p.qtiles * p.bq;
     p.off_fq = 0;
     p.off_gt = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
-    p.off_h = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
-    p.off_ps = align256(p.off_h + sizeof(uint32_t) * 33 * (size_t)p.sample_groups * p.b_pad);
+    p.off_ps = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
     p.bytes = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
     return p;
@@ -540,10 +528,9 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         }
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
-        uint32_t* hist = p.sample_groups > 0 ? reinterpret_cast<uint32_t*>(w + p.off_h) : nullptr;
         if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, s)) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
-        e = launch_qs(p, dt, n, d, emb, fe, q, fq, gt, hist, b, k, ps, pi, s);
+        e = launch_qs(p, dt, n, d, emb, fe, q, fq, gt, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QSTAT) {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qstat(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
