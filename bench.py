@@ -27,6 +27,15 @@ PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0, "e4m3": 5000.0}
 MALL_BYTES = 256 << 20
 
+# HBM bytes per launch of the similarity kernel from the FETCH_SIZE and
+# WRITE_SIZE counters, scaled by a plain copy's readings
+# (profiles/qs_hbm_bytes_all_workloads_pmc.md).  They hold for the kernel and
+# plan sources they were taken on; any other source reports null.
+TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/simtopk.hip")
+TRAFFIC_SHA256 = "0a10e9155fd3842c"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160679589, "b1024_n1m_d768_bf16": 1573859155,
+                 "b4096_n4m_d512_f16": 6837671650, "b16384_n10m_d768_e4m3": 605971447785}
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -58,6 +67,15 @@ class HipEvents:
         for a, b in self.pairs:
             self.hip.hipEventDestroy(a)
             self.hip.hipEventDestroy(b)
+
+
+def measured_traffic(name):
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return TRAFFIC_BYTES.get(name) if h.hexdigest()[:16] == TRAFFIC_SHA256 else None
 
 
 def alg_bytes(w):
@@ -181,11 +199,12 @@ def main():
     if ai < ridge:
         achieved = nbytes / (kern_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic(w.name)}
     else:
         achieved = flops / (kern_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_TFLOPS[w.dtype],
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[w.dtype], 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[w.dtype], 4),
+                "traffic": measured_traffic(w.name)}
 
     out = {
         "metric": METRIC,
