@@ -101,13 +101,110 @@ __global__ __launch_bounds__(NT) void k_assign(const AssignTable t, const float*
         }
 }
 
+// The same with every query's state in registers (thread tid owns queries
+// tid + c NT, c < QPT): no global-memory round trip per round.
+template <int QPT>
+__global__ __launch_bounds__(NT) void k_assign_reg(const AssignTable t, const float* __restrict__ top_score,
+                                                   int32_t ld, int32_t b, int32_t* __restrict__ opt_level,
+                                                   int32_t* __restrict__ out_level,
+                                                   int32_t* __restrict__ out_inst,
+                                                   int32_t* __restrict__ out_slot,
+                                                   int32_t* __restrict__ inst_fill)
+{
+    __shared__ int used[APC_MAX_LEVELS + 1];
+    __shared__ int wcnt[NWAVE][APC_MAX_LEVELS + 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = t.L;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int lam[QPT], lev[QPT], rk[QPT];
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        const int q = c * NT + tid;
+        lam[c] = 0;
+        lev[c] = -1;
+        rk[c] = -1;
+        if (q < b) {
+            const float best = top_score[(int64_t)q * ld];
+            for (int l = 0; l < L; ++l) lam[c] += best >= t.theta[l];
+        }
+    }
+    if (tid <= L) used[tid] = 0;
+    __syncthreads();
+    const int nchunk = (b + NT - 1) / NT;
+    for (int r = 0; r <= L; ++r) {
+#pragma unroll
+        for (int c = 0; c < QPT; ++c) {
+            if (c < nchunk) {                                 // uniform
+                const int q = c * NT + tid;
+                int want = -1;
+                if (q < b && lev[c] < 0) want = r <= lam[c] ? lam[c] - r : r;
+                int pre = 0;
+                for (int p = 0; p <= L; ++p) {
+                    const uint64_t m = __ballot(want == p);
+                    if (want == p) pre = __popcll(m & lt_mask);
+                    if (lane == 0) wcnt[wave][p] = __popcll(m);
+                }
+                __syncthreads();
+                if (want >= 0) {
+                    int rank = used[want] + pre;
+                    for (int w = 0; w < wave; ++w) rank += wcnt[w][want];
+                    if (rank < t.level_cap[want]) {
+                        lev[c] = want;
+                        rk[c] = rank;
+                    }
+                }
+                __syncthreads();
+                if (tid <= L) {
+                    int tot = 0;
+                    for (int w = 0; w < NWAVE; ++w) tot += wcnt[w][tid];
+                    const int u = used[tid] + tot;
+                    used[tid] = u < t.level_cap[tid] ? u : t.level_cap[tid];
+                }
+                __syncthreads();
+            }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        const int q = c * NT + tid;
+        if (q >= b) continue;
+        const int p = lev[c];
+        int inst = -1, slot = -1;
+        if (p >= 0) {
+            for (int j = t.level_first[p]; j < t.level_first[p + 1]; ++j)
+                if (rk[c] < t.ord_cum[j] + t.ord_cap[j]) {
+                    inst = t.ord_inst[j];
+                    slot = rk[c] - t.ord_cum[j];
+                    break;
+                }
+        }
+        opt_level[q] = lam[c];
+        out_level[q] = p;
+        out_inst[q] = inst;
+        out_slot[q] = slot;
+    }
+    for (int p = 0; p <= L; ++p)
+        for (int j = t.level_first[p] + tid; j < t.level_first[p + 1]; j += NT) {
+            int f = used[p] - t.ord_cum[j];
+            f = f < 0 ? 0 : (f > t.ord_cap[j] ? t.ord_cap[j] : f);
+            inst_fill[t.ord_inst[j]] = f;
+        }
+}
+
 }  // namespace
 
 hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t ld, int32_t b,
                          int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
                          int32_t* out_slot, int32_t* inst_fill, hipStream_t s)
 {
-    k_assign<<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    if (b <= NT)
+        k_assign_reg<1><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= 4 * NT)
+        k_assign_reg<4><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= 16 * NT)
+        k_assign_reg<16><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else
+        k_assign<<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     return hipGetLastError();
 }
 
