@@ -236,6 +236,15 @@ __device__ inline void q2_insert_sorted(uint64_t (&lk)[KR], uint64_t key)
     }
 }
 
+// 2 m + c in one instruction: the compare result c enters as the carry
+__device__ inline uint32_t q2_shift_in(uint32_t m, bool c)
+{
+    uint32_t r;
+    uint64_t carry_out;
+    asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry_out) : "v"(m), "s"(__builtin_amdgcn_ballot_w64(c)));
+    return r;
+}
+
 // (m & x) | (~m & y) as one instruction the optimizer cannot restructure
 __device__ inline float q2_bsel(uint32_t m, float x, float y)
 {
@@ -506,6 +515,36 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         const bool whole = e0 + GR <= n;
         const int64_t lim64 = n - e0 - 4 * h;                  // rows 8g + i (+ 32 eb) below this are < n
         const float* fr = sm.fe[gi % Q2_FR];             // the group's entry factors
+        // The filter threshold F is the largest valid lower bound on the query's
+        // k-th best score: the lane's own k-th, its partner lane's, the global one.
+        // The lane's best score in the group is computed exactly: its largest
+        // product times entry factor, then times f_q and clamped (both monotone).
+        // The products times entry factor stay in acc for the exact test below.
+        // Rows past n read the zero padding of the factors, which at most lets
+        // the group through to that test.
+        float m[MQ];
+#pragma unroll
+        for (int mq = 0; mq < MQ; ++mq) m[mq] = neg_inf();
+#pragma unroll
+        for (int eb = 0; eb < EB; ++eb) {
+            float fv[16];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
+                fv[4 * g] = f4.x;
+                fv[4 * g + 1] = f4.y;
+                fv[4 * g + 2] = f4.z;
+                fv[4 * g + 3] = f4.w;
+            }
+#pragma unroll
+            for (int mq = 0; mq < MQ; ++mq)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float x = acc[mq][eb][r] * fv[r];
+                    acc[mq][eb][r] = x;
+                    m[mq] = __builtin_fmaxf(m[mq], x);
+                }
+        }
         if (gi == 0 && k <= 16) {
             // Seed for the first group (the lists are still empty): the 8 EB quads
             // of a lane pair are disjoint, so with m = ceil(k/2), the smaller of
@@ -523,7 +562,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             if (whole || 32 * eb + 8 * g + i < lim64)
-                                x = __builtin_fmaxf(x, acc[mq][eb][4 * g + i] * fr[eb * 32 + 8 * g + 4 * h + i]);
+                                x = __builtin_fmaxf(x, acc[mq][eb][4 * g + i]);
                         qm[4 * eb + g] = x;
                     }
                 // sort descending (bitonic)
@@ -557,31 +596,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 if (ss > ps[mq]) ps[mq] = ss;
             }
         }
-        // The filter threshold F is the largest valid lower bound on the query's
-        // k-th best score: the lane's own k-th, its partner lane's, the global one.
-        // The lane's best score in the group is computed exactly: its largest
-        // product times entry factor, then times f_q and clamped (both monotone).
-        // Rows past n read the zero padding of the factors, which at most lets
-        // the group through to the exact test below.
-        float m[MQ];
-#pragma unroll
-        for (int mq = 0; mq < MQ; ++mq) m[mq] = neg_inf();
-#pragma unroll
-        for (int eb = 0; eb < EB; ++eb) {
-            float fv[16];
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                fv[4 * g] = f4.x;
-                fv[4 * g + 1] = f4.y;
-                fv[4 * g + 2] = f4.z;
-                fv[4 * g + 3] = f4.w;
-            }
-#pragma unroll
-            for (int mq = 0; mq < MQ; ++mq)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) m[mq] = __builtin_fmaxf(m[mq], acc[mq][eb][r] * fv[r]);
-        }
         float G[MQ], F[MQ];
         bool pass[MQ];
         bool any_pass = false;
@@ -593,33 +607,48 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             any_pass |= pass[mq];
         }
         if (__builtin_amdgcn_ballot_w64(any_pass)) {
+            // rows below n, bit 16 eb + r for row 32 eb + 8 (r / 4) + 4 h + r % 4
+            Mask valid = ~(Mask)0;
+            if (!whole) {
+                valid = 0;
+#pragma unroll
+                for (int eb = 0; eb < EB; ++eb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        if (32 * eb + 8 * (r >> 2) + (r & 3) < lim64) valid |= (Mask)1 << (16 * eb + r);
+            }
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
-                // exact scores, and the pairs that reach the filter
+                // the pairs whose exact score reaches F.  Scores are at least -1, so
+                // with F <= -1 every row passes; otherwise clamp1(y) >= F exactly when
+                // y >= F (F <= 1, and a NaN product fails both).  The bits are shifted
+                // in from the highest row of each 32-bit word down.
                 Mask mask = 0;
                 if (pass[mq]) {
+                    if (F[mq] <= -1.f) {
+                        mask = valid;
+                    } else {
+                        uint32_t w[(EB * 16 + 31) / 32];
 #pragma unroll
-                    for (int eb = 0; eb < EB; ++eb)
+                        for (int wi = 0; wi < (EB * 16 + 31) / 32; ++wi) {
+                            uint32_t b = 0;
 #pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            const float4 f4 = *reinterpret_cast<const float4*>(fr + eb * 32 + 8 * g + 4 * h);
-                            const float fv[4] = {f4.x, f4.y, f4.z, f4.w};
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const int r = 4 * g + i;
-                                const float sc = clamp1(acc[mq][eb][r] * fv[i] * fq[mq]);
-                                acc[mq][eb][r] = sc;
-                                const bool ok = (whole || 32 * eb + 8 * g + i < lim64) && sc >= F[mq];
-                                mask |= (Mask)ok << (16 * eb + r);
+                            for (int j = 31; j >= 0; --j) {
+                                const int el = 32 * wi + j;
+                                b = q2_shift_in(b, acc[mq][el >> 4][el & 15] * fq[mq] >= F[mq]);
                             }
+                            w[wi] = b;
                         }
+                        if constexpr (EB == 4) mask = ((Mask)w[1] << 32 | w[0]) & valid;
+                        else mask = w[0] & valid;
+                    }
                 }
                 // every lane inserts into its own list, one pair per pass
                 while (__builtin_amdgcn_ballot_w64(mask != 0)) {
                     const bool act = mask != 0;
                     const int bsel = act ? (EB == 4 ? __builtin_ctzll((uint64_t)mask) : __builtin_ctz((uint32_t)mask)) : 0;
                     mask &= mask - 1;
-                    const float sc = q2_pick<EB>(acc[mq], bsel);
+                    const float sc = clamp1(q2_pick<EB>(acc[mq], bsel) * fq[mq]);
                     const int r = bsel & 15;
                     const int e = (int)(e0 + 32 * (bsel >> 4) + 8 * (r >> 2) + 4 * h + (r & 3));
                     const uint64_t key = q2_pack(sc, e);
