@@ -683,21 +683,25 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     // merge it with the partner lane's, lane half 0 writes the k best ----
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
-        uint64_t x[KR];
+        // the list padded with empty slots to a power of two
+        constexpr int KP = KR <= 16 ? 16 : 32;
+        uint64_t x[KP];
 #pragma unroll
-        for (int p = 0; p < KR; ++p) {
-            uint64_t v;
-            if constexpr (LREG) v = lk[mq][p];
-            else v = lcol[mq][p * 64];
+        for (int p = 0; p < KP; ++p) {
+            uint64_t v = 0ull;
+            if (p < KR) {
+                if constexpr (LREG) v = lk[mq][p];
+                else v = lcol[mq][p * 64];
+            }
             x[p] = v == ~0ull ? 0ull : v;
         }
         // bitonic sort, descending (register lists are sorted already)
 #pragma unroll
-        for (int size = 2; size <= (LREG ? 1 : KR); size *= 2)
+        for (int size = 2; size <= (LREG ? 1 : KP); size *= 2)
 #pragma unroll
             for (int stride = size / 2; stride > 0; stride /= 2)
 #pragma unroll
-                for (int i = 0; i < KR; ++i) {
+                for (int i = 0; i < KP; ++i) {
                     const int j = i ^ stride;
                     if (j > i) {
                         const bool desc = (i & size) == 0;
@@ -707,20 +711,20 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                         x[j] = sw ? a0 : a1;
                     }
                 }
-        // the larger of own[p] and partner[KR - 1 - p] is a bitonic sequence
-        // holding the KR largest of both lists; half-cleaners sort it
-        uint64_t m[KR];
+        // the larger of own[p] and partner[KP - 1 - p] is a bitonic sequence
+        // holding the KP largest of both lists; half-cleaners sort it
+        uint64_t m[KP];
 #pragma unroll
-        for (int p = 0; p < KR; ++p) {
-            const uint64_t o = x[KR - 1 - p];
+        for (int p = 0; p < KP; ++p) {
+            const uint64_t o = x[KP - 1 - p];
             const uint32_t lo = __shfl_xor((uint32_t)o, 32, 64), hi = __shfl_xor((uint32_t)(o >> 32), 32, 64);
-            const uint64_t y = ((uint64_t)hi << 32) | lo;            // partner's (KR - 1 - p)-th
+            const uint64_t y = ((uint64_t)hi << 32) | lo;            // partner's (KP - 1 - p)-th
             m[p] = x[p] > y ? x[p] : y;
         }
 #pragma unroll
-        for (int stride = KR / 2; stride > 0; stride /= 2)
+        for (int stride = KP / 2; stride > 0; stride /= 2)
 #pragma unroll
-            for (int i = 0; i < KR; ++i)
+            for (int i = 0; i < KP; ++i)
                 if ((i & stride) == 0) {
                     const bool sw = m[i] < m[i + stride];
                     const uint64_t a0 = m[i], a1 = m[i + stride];
@@ -755,8 +759,10 @@ hipError_t run_qs(const MatchPlan& p, int64_t n, const void* emb, const float* f
 }  // namespace
 
 // shape of the query-stationary kernel: rows of 512, 768, 1024 or 1536 bytes,
-// k <= 32.  Lists of 16 slots for k <= 16 (two query blocks per wavefront
-// except for 1536-byte rows), of 32 slots otherwise (one query block).
+// k <= 32.  Lists of 10 slots for k <= 10, 16 for k <= 16 (two query blocks
+// per wavefront except for 1536-byte rows), 32 otherwise (one query block).
+// Every insertion touches every slot, so the list is kept close to k.
+constexpr int q2_kr(int k) { return k <= 10 ? 10 : k <= 16 ? 16 : 32; }
 constexpr int q2_mq(int64_t row_bytes, int k) { return k <= 16 && row_bytes != 1536 ? 2 : 1; }
 // 32-row blocks per stage and group: four with one query block (two where
 // 1536-byte rows and 32-slot lists leave too few registers), two with two
@@ -777,7 +783,14 @@ hipError_t q2_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* em
                        const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
 #define APC_Q2(RB, MQ, KR) run_qs<DT, RB, MQ, KR, q2_eb(RB, KR)>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s)
-    if (k <= 16) {
+    if (q2_kr(k) == 10) {
+        switch (rb) {
+        case 1536: return APC_Q2(1536, 1, 10);
+        case 1024: return APC_Q2(1024, 2, 10);
+        case 768: return APC_Q2(768, 2, 10);
+        case 512: return APC_Q2(512, 2, 10);
+        }
+    } else if (q2_kr(k) == 16) {
         switch (rb) {
         case 1536: return APC_Q2(1536, 1, 16);
         case 1024: return APC_Q2(1024, 2, 16);

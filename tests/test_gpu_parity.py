@@ -97,8 +97,8 @@ CASES = [
     ("f16", 64, 1000, 1536, 12),
     # query-stationary kernel: 16-bit or e4m3 rows of 512, 768, 1024 or 1536
     # bytes, k <= 32; every shape family (rows, query blocks, 32-row blocks per
-    # group, lists in registers or LDS), with and without the sampling pass
-    ("e4m3", 100, 2050, 768, 10),      # 768 B, two query blocks, sampling pass
+    # group, lists of 10, 16 or 32 slots in registers or LDS)
+    ("e4m3", 100, 2050, 768, 10),      # 768 B, two query blocks, 10-slot lists
     ("f16", 256, 7777, 768, 10),       # 1536 B, one block, four 32-row blocks
     ("bf16", 3, 17, 256, 17),          # one group, one split
     ("f16", 5, 40, 256, 3),
@@ -109,7 +109,7 @@ CASES = [
     ("e4m3", 300, 9000, 768, 10),
     ("f16", 1, 31, 768, 5),
     ("f16", 40, 100, 512, 7),          # 1024 B, lists in LDS
-    ("e4m3", 5, 70000, 512, 16),       # 512 B, two query blocks, sampling pass
+    ("e4m3", 5, 70000, 512, 16),       # 512 B, two query blocks, 16-slot lists
     ("bf16", 512, 20000, 256, 8),
     ("f16", 200, 40000, 256, 3),
     ("f16", 150, 6000, 256, 12),       # 512 B, two query blocks
@@ -119,6 +119,10 @@ CASES = [
     ("e4m3", 90, 5000, 1024, 20),      # 1024 B e4m3, one block, 32-slot lists
     ("e4m3", 33, 4000, 1536, 11),      # 1536 B e4m3, one block, four 32-row blocks
     ("bf16", 64, 3000, 768, 29),       # 1536 B, 32-slot lists
+    ("e4m3", 40, 5000, 1536, 6),       # 1536 B e4m3, 10-slot lists
+    ("e4m3", 70, 6000, 1024, 10),      # 1024 B e4m3, two query blocks, 10-slot lists in LDS
+    ("f16", 80, 5000, 512, 14),        # 1024 B, 16-slot lists in LDS
+    ("f16", 130, 9000, 768, 11),       # 1536 B, 16-slot lists just above 10
 ]
 
 
@@ -153,9 +157,9 @@ def test_match_small(apc, orc, dtype, b, n, d, k):
 
 @pytest.mark.parametrize("dtype,b,n,d,k", [("f16", 2048, 40000, 768, 10), ("e4m3", 1024, 60000, 512, 12)])
 def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
-    """Enough query tiles that each split holds many groups: no sampling pass,
-    lists fill and bounds tighten as the pass goes; a subset of rows is checked."""
-    say(f"match (no sampling pass) {dtype} b={b} n={n} d={d} k={k}")
+    """Enough query tiles that each split holds many groups: lists fill and
+    bounds tighten as the pass goes; a subset of rows is checked."""
+    say(f"match (many groups per split) {dtype} b={b} n={n} d={d} k={k}")
     e, es = make_rows(n, d, dtype, 30 + n, clusters=max(1, n // 50))
     q, qs = make_rows(b, d, dtype, 40 + b, clusters=None)
     q[: b // 2] = e[torch.arange(b // 2, device="cuda") * 13 % n]
