@@ -28,11 +28,16 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          # MFMA results in VGPRs: no copies of the accumulators between register files
          "-mllvm", "-amdgpu-mfma-vgpr-form"]
+# Per-source additions.  The query-stationary kernels keep their per-lane lists
+# as separate registers: promoted to one vector, a list is copied whole on
+# every pass of the insertion loop.
+SOURCE_FLAGS = {src: ["-mllvm", "-disable-promote-alloca-to-vector"]
+                for src in ("qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip")}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
@@ -41,7 +46,8 @@ def _compile(src: str) -> str:
 
 def _check_no_scratch(src: str) -> None:
     asm = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
-    cmd = [HIPCC, *FLAGS, "--cuda-device-only", "-S", "-x", "hip", os.path.join(CSRC, src), "-o", asm]
+    cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), "--cuda-device-only", "-S", "-x", "hip",
+           os.path.join(CSRC, src), "-o", asm]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")

@@ -218,22 +218,19 @@ __device__ inline void q2_worst(const uint64_t* col, uint64_t& wkey, int& wp)
 }
 
 // register form, kept sorted by key descending: insert key (0 inserts
-// nothing), dropping the smallest; every slot compares once and shifts down
-// when the key goes above the slot before it
+// nothing), dropping the smallest.  Every slot compares once; a slot takes the
+// one before it when the key goes above that one, the key when it goes above
+// only this one.  Slots are written from the last up, so each new value can
+// take the old one's register.
 template <int KR>
 __device__ inline void q2_insert_sorted(uint64_t (&lk)[KR], uint64_t key)
 {
-    uint64_t prev = lk[0];
-    bool above_prev = key > prev;
-    lk[0] = above_prev ? key : prev;
+    bool above[KR];
 #pragma unroll
-    for (int p = 1; p < KR; ++p) {
-        const uint64_t cur = lk[p];
-        const bool above = key > cur;
-        lk[p] = above_prev ? prev : (above ? key : cur);
-        prev = cur;
-        above_prev = above;
-    }
+    for (int p = 0; p < KR; ++p) above[p] = key > lk[p];
+#pragma unroll
+    for (int p = KR - 1; p > 0; --p) lk[p] = above[p - 1] ? lk[p - 1] : (above[p] ? key : lk[p]);
+    lk[0] = above[0] ? key : lk[0];
 }
 
 // 2 m + c in one instruction: the compare result c enters as the carry
@@ -245,12 +242,18 @@ __device__ inline uint32_t q2_shift_in(uint32_t m, bool c)
     return r;
 }
 
-// (m & x) | (~m & y) as one instruction the optimizer cannot restructure
+// (m & x) | (~m & y) for a mask m of all zeros or all ones (one v_bfi_b32).
+// The mask goes through an empty asm so that the optimizer cannot see it is
+// a select and fold a tree of them into one dynamically indexed read, which
+// would go through scratch memory.
+__device__ inline uint32_t q2_opaque(uint32_t m)
+{
+    asm("" : "+v"(m));
+    return m;
+}
 __device__ inline float q2_bsel(uint32_t m, float x, float y)
 {
-    float r;
-    asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(x), "v"(y));
-    return r;
+    return __uint_as_float((__float_as_uint(x) & m) | (__float_as_uint(y) & ~m));
 }
 
 // slot i (the same for the whole wavefront, below KR) of a register list,
@@ -266,7 +269,7 @@ __device__ inline uint64_t q2_slot(const uint64_t (&lk)[KR], int i)
     }
 #pragma unroll
     for (int w = 1; w < KR; w *= 2) {
-        const uint32_t m = 0u - (uint32_t)((i / w) & 1);
+        const uint32_t m = q2_opaque(0u - (uint32_t)((i / w) & 1));
 #pragma unroll
         for (int p = 0; p + w < KR; p += 2 * w) {
             lo[p] = __float_as_uint(q2_bsel(m, __uint_as_float(lo[p + w]), __uint_as_float(lo[p])));
@@ -282,15 +285,16 @@ __device__ inline uint64_t q2_slot(const uint64_t (&lk)[KR], int i)
 template <int EB>
 __device__ inline float q2_pick(const f32x16 (&v)[EB], int b)
 {
-    const uint32_t m0 = 0u - (uint32_t)(b & 1), m1 = 0u - (uint32_t)((b >> 1) & 1), m2 = 0u - (uint32_t)((b >> 2) & 1);
-    const uint32_t m3 = 0u - (uint32_t)((b >> 3) & 1), m4 = 0u - (uint32_t)((b >> 4) & 1);
+    const uint32_t m0 = q2_opaque(0u - (uint32_t)(b & 1)), m1 = q2_opaque(0u - (uint32_t)((b >> 1) & 1));
+    const uint32_t m2 = q2_opaque(0u - (uint32_t)((b >> 2) & 1)), m3 = q2_opaque(0u - (uint32_t)((b >> 3) & 1));
+    const uint32_t m4 = q2_opaque(0u - (uint32_t)((b >> 4) & 1));
     float l16[16], l8[8], l4[4];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
         if constexpr (EB == 2) {
             l16[i] = q2_bsel(m4, v[1][i], v[0][i]);
         } else {
-            const uint32_t m5 = 0u - (uint32_t)((b >> 5) & 1);
+            const uint32_t m5 = q2_opaque(0u - (uint32_t)((b >> 5) & 1));
             l16[i] = q2_bsel(m5, q2_bsel(m4, v[3][i], v[2][i]), q2_bsel(m4, v[1][i], v[0][i]));
         }
     }
