@@ -20,7 +20,27 @@ namespace {
 constexpr int NT = 1024;
 constexpr int NWAVE = NT / 64;
 
-__global__ __launch_bounds__(NT) void k_assign(const AssignTable t, const float* __restrict__ top_score,
+// The table is a kernel argument.  Kernel-argument memory is read through
+// uncached paths, so every per-lane (dynamically indexed) read of it would be
+// a full memory round trip; the kernels copy it into LDS once instead.
+// All of a thread's loads are issued before its stores: one round trip.
+static_assert(sizeof(AssignTable) % 4 == 0, "table copied as 32-bit words");
+template <int NTHR>
+__device__ inline void table_to_lds(const AssignTable& src, AssignTable& dst, int tid)
+{
+    constexpr int W = (int)(sizeof(AssignTable) / 4), PER = (W + NTHR - 1) / NTHR;
+    const uint32_t* s = reinterpret_cast<const uint32_t*>(&src);
+    uint32_t* d = reinterpret_cast<uint32_t*>(&dst);
+    uint32_t v[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v[i] = tid + i * NTHR < W ? s[tid + i * NTHR] : 0u;
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+        if (tid + i * NTHR < W) d[tid + i * NTHR] = v[i];
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(NT) void k_assign(const AssignTable targ, const float* __restrict__ top_score,
                                                 int32_t ld, int32_t b, int32_t* __restrict__ opt_level,
                                                 int32_t* __restrict__ out_level,
                                                 int32_t* __restrict__ out_inst,
@@ -29,7 +49,9 @@ __global__ __launch_bounds__(NT) void k_assign(const AssignTable t, const float*
 {
     __shared__ int used[APC_MAX_LEVELS + 1];
     __shared__ int wcnt[NWAVE][APC_MAX_LEVELS + 1];
+    __shared__ AssignTable t;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    table_to_lds<NT>(targ, t, tid);
     const int L = t.L;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
@@ -102,18 +124,32 @@ __global__ __launch_bounds__(NT) void k_assign(const AssignTable t, const float*
 }
 
 // The same with every query's state in registers (thread tid owns queries
-// tid + c NT, c < QPT): no global-memory round trip per round.
-template <int QPT>
-__global__ __launch_bounds__(NT) void k_assign_reg(const AssignTable t, const float* __restrict__ top_score,
-                                                   int32_t ld, int32_t b, int32_t* __restrict__ opt_level,
-                                                   int32_t* __restrict__ out_level,
-                                                   int32_t* __restrict__ out_inst,
-                                                   int32_t* __restrict__ out_slot,
-                                                   int32_t* __restrict__ inst_fill)
+// tid + c NTB, c < QPT): no global-memory round trip per round.  The block
+// is sized to the batch (NTB threads).  Each chunk of a round takes two
+// barriers: after the per-wave ballots, and after the ranks, which read the
+// level counts of the round so far (used[cur]) while threads p <= L write the
+// counts after this chunk into the other buffer.  The rounds stop once a round
+// has no applicant (every query placed; later rounds would change nothing).
+template <int QPT, int NTB>
+__global__ __launch_bounds__(NTB) void k_assign_reg(const AssignTable targ, const float* __restrict__ top_score,
+                                                    int32_t ld, int32_t b, int32_t* __restrict__ opt_level,
+                                                    int32_t* __restrict__ out_level,
+                                                    int32_t* __restrict__ out_inst,
+                                                    int32_t* __restrict__ out_slot,
+                                                    int32_t* __restrict__ inst_fill)
 {
-    __shared__ int used[APC_MAX_LEVELS + 1];
-    __shared__ int wcnt[NWAVE][APC_MAX_LEVELS + 1];
+    constexpr int NT = NTB, NWAVE = NTB / 64;
+    __shared__ int used[2][APC_MAX_LEVELS + 1];
+    __shared__ int wcnt[NWAVE][APC_MAX_LEVELS + 2];          // [L + 1]: the wave has an applicant
+    __shared__ AssignTable t;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float best[QPT];
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {                          // issued before the table copy
+        const int q = c * NT + tid;
+        best[c] = q < b ? top_score[(int64_t)q * ld] : 0.f;
+    }
+    table_to_lds<NT>(targ, t, tid);
     const int L = t.L;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int lam[QPT], lev[QPT], rk[QPT];
@@ -123,15 +159,14 @@ __global__ __launch_bounds__(NT) void k_assign_reg(const AssignTable t, const fl
         lam[c] = 0;
         lev[c] = -1;
         rk[c] = -1;
-        if (q < b) {
-            const float best = top_score[(int64_t)q * ld];
-            for (int l = 0; l < L; ++l) lam[c] += best >= t.theta[l];
-        }
+        if (q < b)
+            for (int l = 0; l < L; ++l) lam[c] += best[c] >= t.theta[l];
     }
-    if (tid <= L) used[tid] = 0;
-    __syncthreads();
+    if (tid <= L) used[0][tid] = 0;
+    int cur = 0;
     const int nchunk = (b + NT - 1) / NT;
     for (int r = 0; r <= L; ++r) {
+        bool round_any = false;
 #pragma unroll
         for (int c = 0; c < QPT; ++c) {
             if (c < nchunk) {                                 // uniform
@@ -144,25 +179,38 @@ __global__ __launch_bounds__(NT) void k_assign_reg(const AssignTable t, const fl
                     if (want == p) pre = __popcll(m & lt_mask);
                     if (lane == 0) wcnt[wave][p] = __popcll(m);
                 }
+                const bool wave_any = __ballot(want >= 0) != 0;
+                if (lane == 0) wcnt[wave][L + 1] = wave_any;
                 __syncthreads();
+                bool any = false;
+#pragma unroll
+                for (int w = 0; w < NWAVE; ++w) any |= wcnt[w][L + 1] != 0;
+                if (!any) {                                   // uniform: no applicant in this chunk
+                    __syncthreads();                          // before the next chunk rewrites wcnt
+                    continue;
+                }
+                round_any = true;
                 if (want >= 0) {
-                    int rank = used[want] + pre;
-                    for (int w = 0; w < wave; ++w) rank += wcnt[w][want];
+                    int rank = used[cur][want] + pre;
+#pragma unroll
+                    for (int w = 0; w < NWAVE; ++w) rank += w < wave ? wcnt[w][want] : 0;
                     if (rank < t.level_cap[want]) {
                         lev[c] = want;
                         rk[c] = rank;
                     }
                 }
-                __syncthreads();
                 if (tid <= L) {
-                    int tot = 0;
+                    int tot = used[cur][tid];
+#pragma unroll
                     for (int w = 0; w < NWAVE; ++w) tot += wcnt[w][tid];
-                    const int u = used[tid] + tot;
-                    used[tid] = u < t.level_cap[tid] ? u : t.level_cap[tid];
+                    const int cap = t.level_cap[tid];
+                    used[cur ^ 1][tid] = tot < cap ? tot : cap;
                 }
                 __syncthreads();
+                cur ^= 1;
             }
         }
+        if (!round_any) break;                                // uniform
     }
 #pragma unroll
     for (int c = 0; c < QPT; ++c) {
@@ -185,7 +233,7 @@ __global__ __launch_bounds__(NT) void k_assign_reg(const AssignTable t, const fl
     }
     for (int p = 0; p <= L; ++p)
         for (int j = t.level_first[p] + tid; j < t.level_first[p + 1]; j += NT) {
-            int f = used[p] - t.ord_cum[j];
+            int f = used[cur][p] - t.ord_cum[j];
             f = f < 0 ? 0 : (f > t.ord_cap[j] ? t.ord_cap[j] : f);
             inst_fill[t.ord_inst[j]] = f;
         }
@@ -197,12 +245,14 @@ hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t l
                          int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
                          int32_t* out_slot, int32_t* inst_fill, hipStream_t s)
 {
-    if (b <= NT)
-        k_assign_reg<1><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    if (b <= 256)
+        k_assign_reg<1, 256><<<1, 256, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= NT)
+        k_assign_reg<1, NT><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     else if (b <= 4 * NT)
-        k_assign_reg<4><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+        k_assign_reg<4, NT><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     else if (b <= 16 * NT)
-        k_assign_reg<16><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
+        k_assign_reg<16, NT><<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     else
         k_assign<<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     return hipGetLastError();

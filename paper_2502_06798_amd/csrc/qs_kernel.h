@@ -737,7 +737,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 }
         const int64_t qg = q0w + mq * 32 + r32;
         if (h == 0 && qg < b_pad) {
-            const int64_t o = ((int64_t)split * b_pad + qg) * k;
+            const int64_t o = (qg * splits + split) * k;
 #pragma unroll
             for (int p = 0; p < KR; ++p)
                 if (p < k) {

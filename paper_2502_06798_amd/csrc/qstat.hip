@@ -424,7 +424,7 @@ __global__ __launch_bounds__(QS_NT) void k_qstat(
         list_merge_partner(ls[mq], li[mq]);
         const int64_t qg = q0 + mq * 32 + r32;
         if (h == 0 && qg < b_pad) {
-            const int64_t o = ((int64_t)split * b_pad + qg) * k;
+            const int64_t o = ((int64_t)qg * splits + split) * k;
 #pragma unroll
             for (int p = 0; p < QS_KR; ++p)
                 if (p < k) {

@@ -332,13 +332,55 @@ __global__ __launch_bounds__(WQ * WE * 64) void k_simtopk(
     __syncthreads();
     for (int i = tid; i < BQ * k; i += P::NT) {
         const int qi = i / k, p = i % k;
-        const int64_t o = ((int64_t)split * b_pad + q0 + qi) * k + p;
+        const int64_t o = (((int64_t)q0 + qi) * splits + split) * k + p;
         part_s[o] = sm.list_s[p * BQ + qi];
         part_i[o] = sm.list_i[p * BQ + qi];
     }
 }
 
 // ---- merge of the per-split partial lists ----------------------------------
+// (score, index) as one key ordered like (score desc, index asc): the score's
+// bits mapped to an order-preserving unsigned integer, then the complement of
+// the index.  Adding +0 turns -0 into +0, which compare equal as scores.
+__device__ inline uint64_t merge_key(float s, int i)
+{
+    const uint32_t u = __float_as_uint(s + 0.0f);
+    const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)i;
+}
+__device__ inline float merge_key_score(uint64_t key)
+{
+    const uint32_t o = (uint32_t)(key >> 32);
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+// one step of a wavefront maximum: the key of the lane that the DPP control
+// names (own key where it names none, or the row is masked off)
+template <int CTRL, int ROWS>
+__device__ inline uint64_t dpp_max_step(uint64_t v)
+{
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+    const uint32_t olo = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xf, false);
+    const uint32_t ohi = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xf, false);
+    const uint64_t o = ((uint64_t)ohi << 32) | olo;
+    return o > v ? o : v;
+}
+// largest key of the wavefront, in every lane: quads (xor 1, xor 2), half
+// rows (mirror), rows (mirror), then rows 1 and 3 take row 0's and row 2's
+// maximum (broadcast of lane 15) and rows 2 and 3 row 1's (lane 31): lane 63
+// ends with the maximum of all 64 lanes
+__device__ inline uint64_t wave_max_key(uint64_t v)
+{
+    v = dpp_max_step<0xB1, 0xf>(v);      // quad_perm [1, 0, 3, 2]
+    v = dpp_max_step<0x4E, 0xf>(v);      // quad_perm [2, 3, 0, 1]
+    v = dpp_max_step<0x141, 0xf>(v);     // row_half_mirror
+    v = dpp_max_step<0x140, 0xf>(v);     // row_mirror
+    v = dpp_max_step<0x142, 0xa>(v);     // row_bcast:15
+    v = dpp_max_step<0x143, 0xc>(v);     // row_bcast:31
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 template <int MAXOWN>
 __global__ __launch_bounds__(256) void k_topk_merge(const float* __restrict__ part_s,
                                                      const int* __restrict__ part_i, int splits,
@@ -357,6 +399,15 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float* __restrict__ pa
         }
         return;
     }
+    const int ne = splits * k;                                     // this query's entries
+    const float* gs = part_s + (int64_t)q * ne;
+    const int* gi = part_i + (int64_t)q * ne;
+    // a lane's list heads advance by loads from this query's block, which the
+    // first loads bring into the vector cache
+    auto fetch = [&](int l, int hd, float& sc, int& ix) {
+        sc = gs[l * k + hd];
+        ix = gi[l * k + hd];
+    };
     int head[MAXOWN];
     float cs[MAXOWN];
     int ci[MAXOWN];
@@ -365,9 +416,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float* __restrict__ pa
         const int l = lane + 64 * j;
         head[j] = 0;
         if (l < splits) {
-            const int64_t o = ((int64_t)l * b_pad + q) * k;
-            cs[j] = part_s[o];
-            ci[j] = part_i[o];
+            fetch(l, 0, cs[j], ci[j]);
         } else {
             cs[j] = neg_inf();
             ci[j] = IDX_NONE;
@@ -379,14 +428,9 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float* __restrict__ pa
 #pragma unroll
         for (int j = 1; j < MAXOWN; ++j)
             if (before(cs[j], ci[j], bs, bi)) { bs = cs[j]; bi = ci[j]; bj = j; }
-        float ws = bs;
-        int wi = bi;
-#pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) {
-            const float os = __shfl_xor(ws, m, 64);
-            const int oi = __shfl_xor(wi, m, 64);
-            if (before(os, oi, ws, wi)) { ws = os; wi = oi; }
-        }
+        const uint64_t wk = wave_max_key(merge_key(bs, bi));
+        const float ws = merge_key_score(wk);
+        const int wi = (int)~(uint32_t)wk;
         if (lane == 0) {
             top_s[q * k + p] = ws;
             top_i[q * k + p] = wi == IDX_NONE ? -1 : wi;
@@ -398,9 +442,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(const float* __restrict__ pa
                     ++head[j];
                     const int l = lane + 64 * j;
                     if (head[j] < k) {
-                        const int64_t o = ((int64_t)l * b_pad + q) * k + head[j];
-                        cs[j] = part_s[o];
-                        ci[j] = part_i[o];
+                        fetch(l, head[j], cs[j], ci[j]);
                     } else {
                         cs[j] = neg_inf();
                         ci[j] = IDX_NONE;

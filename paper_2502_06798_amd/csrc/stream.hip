@@ -437,7 +437,7 @@ __global__ __launch_bounds__(NW * 64) void k_stream(
 
     if constexpr (REG_LISTS) {
         if (tid < BQ) {
-            const int64_t o = ((int64_t)split * b_pad + q0 + tid) * k;
+            const int64_t o = (((int64_t)q0 + tid) * splits + split) * k;
 #pragma unroll
             for (int p = 0; p < KR; ++p)
                 if (p < k) {
@@ -448,7 +448,7 @@ __global__ __launch_bounds__(NW * 64) void k_stream(
     } else {
         for (int i = tid; i < BQ * k; i += NT) {
             const int q = i / k, p = i % k;
-            const int64_t o = ((int64_t)split * b_pad + q0 + q) * k + p;
+            const int64_t o = (((int64_t)q0 + q) * splits + split) * k + p;
             part_s[o] = st.list_s[st.cur[q]][p * BQ + q];
             part_i[o] = st.list_i[st.cur[q]][p * BQ + q];
         }

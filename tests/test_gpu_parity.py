@@ -240,7 +240,8 @@ def _random_table(rng, L, I, cap_hi=6):
     return il, ic, iq
 
 
-@pytest.mark.parametrize("b,L,I", [(1, 0, 1), (16, 5, 2), (300, 5, 8), (2500, 10, 40), (5000, 32, 256)])
+@pytest.mark.parametrize("b,L,I", [(1, 0, 1), (16, 5, 2), (64, 3, 3), (65, 5, 4), (200, 5, 4), (256, 5, 4),
+                                    (130, 32, 20), (300, 5, 8), (2500, 10, 40), (5000, 32, 256)])
 def test_assign_bit_exact(apc, orc, b, L, I):
     say(f"assign b={b} L={L} I={I}")
     rng = np.random.default_rng(b + L + I)
