@@ -7,21 +7,42 @@ namespace {
 
 // query factors f = 1/|q| (NaN for rows that cannot be matched: non-finite,
 // zero norm, bad e4m3 scale, or padding) and reset global bounds, one
-// wavefront per padded query row
+// wavefront per padded query row.  The row's 16-byte units also go to qperm
+// in the order k_qs loads them (zeros for padding rows): row r of query tile
+// r / bq is query block mq of wavefront w in that tile, lane h 32 + r % 32
+// loads at its step s the units of byte offsets 128 (s UPS / 4) + 64 h +
+// 16 ((s UPS + i) % 4), i < UPS, and those sit at unit
+// ((((tile NW + w) MQ + mq) QST + s) 64 + lane) UPS + i of qperm, so that a
+// wavefront's load of one step reads 64 UPS consecutive units.
 template <int DT>
 __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, const float* __restrict__ q_scale,
                                                 int32_t b, int64_t b_pad, int64_t row_bytes,
-                                                float* __restrict__ fq, int* __restrict__ gthr)
+                                                float* __restrict__ fq, int* __restrict__ gthr,
+                                                uint8_t* __restrict__ qperm, int bq)
 {
+    constexpr int UPS = Q2Op<DT>::UPS;
     const int lane = threadIdx.x & 63;
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (r >= b_pad) return;
+    const int bqw = bq / Q2_NW, mqn = bqw / 32;                // queries per wavefront, blocks
+    const int64_t tile = r / bq;
+    const int local = (int)(r - tile * bq);
+    const int w = local / bqw, mq = (local % bqw) / 32, r32 = local & 31;
+    const int64_t qst = row_bytes / (32 * UPS);
+    uint8_t* tp = qperm + ((((tile * Q2_NW + w) * mqn + mq) * qst) * 64 + r32) * (UPS * 16);
     float ss = 0.f;
     bool bad = false;
-    if (r < b) {
-        const uint8_t* row = qry + r * row_bytes;
-        for (int64_t off = (int64_t)lane * 16; off < row_bytes; off += 64 * 16)
-            sumsq16<DT>(*reinterpret_cast<const uint4*>(row + off), ss, bad);
+    const uint8_t* row = qry + r * row_bytes;
+    for (int64_t off = (int64_t)lane * 16; off < row_bytes; off += 64 * 16) {
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (r < b) {
+            v = *reinterpret_cast<const uint4*>(row + off);
+            sumsq16<DT>(v, ss, bad);
+        }
+        const int64_t u = (off >> 7) * 4 + ((off >> 4) & 3);     // unit within its half-row order
+        const int h = (int)((off >> 6) & 1);
+        const int64_t st = u / UPS, piece = u % UPS;
+        *reinterpret_cast<uint4*>(tp + (st * 64 + h * 32) * (UPS * 16) + piece * 16) = v;
     }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
@@ -48,15 +69,15 @@ int qs_max_k() { return Q2_KMAX; }
 int qs_group_rows(int64_t row_bytes, int k) { return q2_rows(row_bytes, k); }
 
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, hipStream_t s)
+                        float* fq, int* gthr, uint8_t* qperm, int bq, hipStream_t s)
 {
     const dim3 grid((unsigned)((b_pad + 3) / 4)), block(256);
     const uint8_t* qp = static_cast<const uint8_t*>(q);
     switch (dt) {
-    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
-    default: k_qprep<APC_F32><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr); break;
+    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq); break;
+    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq); break;
+    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq); break;
+    default: return hipErrorInvalidValue;                          // the query-stationary kernel takes 16-bit or e4m3 rows
     }
     return hipGetLastError();
 }

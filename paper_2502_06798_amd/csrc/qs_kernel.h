@@ -397,17 +397,16 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     });
 
     // ---- queries into VGPRs, factors, empty lists ----
+    // The queries come in load order (written by the query preparation):
+    // block mq of this wavefront, step s, is 64 consecutive Steps, one per lane.
     Step qv[C::QST][MQ];
     float fq[MQ];
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
         const int64_t qg = q0w + mq * 32 + r32;
-        const uint8_t* qrow = qry + (qg < b ? qg : 0) * RB + h * 64;
+        const uint8_t* qblk = qry + ((((int64_t)qtile * Q2_NW + wave) * MQ + mq) * C::QST * 64 + lane) * sizeof(Step);
 #pragma unroll
-        for (int s = 0; s < C::QST; ++s) {
-            const int u = s * UPS;
-            qv[s][mq] = *reinterpret_cast<const Step*>(qrow + (u / 4) * 128 + (u % 4) * 16);
-        }
+        for (int s = 0; s < C::QST; ++s) qv[s][mq] = *reinterpret_cast<const Step*>(qblk + (int64_t)s * 64 * sizeof(Step));
         fq[mq] = fq_ws[qg];                          // NaN for rows that cannot be matched
     }
     // The compiler waits for these loads here: every value is used by an empty

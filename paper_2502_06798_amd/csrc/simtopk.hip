@@ -543,7 +543,9 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     p.off_gt = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
     p.off_ps = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
-    p.bytes = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
+    p.off_qp = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
+    const size_t qp_bytes = p.kernel == KERNEL_QS ? (size_t)p.b_pad * (size_t)d * elem_bytes(dt) : 0;
+    p.bytes = align256(p.off_qp + qp_bytes);
     return p;
 }
 
@@ -570,9 +572,10 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         }
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
-        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, s)) != hipSuccess) return e;
+        uint8_t* qp = w + p.off_qp;
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, s)) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
-        e = launch_qs(p, dt, n, d, emb, fe, q, fq, gt, b, k, ps, pi, s);
+        e = launch_qs(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QSTAT) {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qstat(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
