@@ -164,15 +164,19 @@ struct Q2Cfg {
     };
 };
 
+// c += a b; first: c = a b (the accumulator input is the constant 0, so the
+// accumulators need no clearing between groups; first is a constant once the
+// step loops are unrolled)
 template <int DT>
-__device__ inline void q2_mma(f32x16& c, const typename Q2Op<DT>::Step a, const typename Q2Op<DT>::Step b)
+__device__ inline void q2_mma(f32x16& c, const typename Q2Op<DT>::Step a, const typename Q2Op<DT>::Step b, bool first)
 {
+    const f32x16 cin = first ? f32x16{} : c;
     if constexpr (DT == APC_F16)
-        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), cin, 0, 0, 0);
     else if constexpr (DT == APC_BF16)
-        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), cin, 0, 0, 0);
     else
-        c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, cin, 0, 0, 0, 0, 0, 0);
 }
 
 // A (score, entry) pair as one 64-bit key ordered like (score desc, entry
@@ -445,13 +449,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         ps[mq] = neg_inf();
     }
 
-    f32x16 acc[MQ][EB];
-#pragma unroll
-    for (int mq = 0; mq < MQ; ++mq)
-#pragma unroll
-        for (int eb = 0; eb < EB; ++eb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
+    f32x16 acc[MQ][EB];      // written whole by each group's first MFMA step
 
     // the stages of logical group gi (every wavefront, for the loads and barriers)
     auto run_group = [&](int gi) __attribute__((always_inline)) {
@@ -499,7 +497,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 #pragma unroll
                 for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
-                    for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[ss][eb], qv[j * SST + ss][mq]);
+                    for (int mq = 0; mq < MQ; ++mq) q2_mma<DT>(acc[mq][eb], a[ss][eb], qv[j * SST + ss][mq], j == 0 && ss == 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
         });
@@ -673,12 +671,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
             const float best = __builtin_fmaxf(own, ps[mq]);
             if (h == 0 && best > G[mq]) q2_atomic_max(gthr + q0w + mq * 32 + r32, q2_key(best));
         }
-#pragma unroll
-        for (int mq = 0; mq < MQ; ++mq)
-#pragma unroll
-            for (int eb = 0; eb < EB; ++eb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[mq][eb][r] = 0.f;
     }
 
     if (!live) return;
