@@ -33,10 +33,11 @@ MALL_BYTES = 256 << 20
 # WRITE_SIZE counters, scaled by a plain copy's readings
 # (profiles/qs_hbm_bytes_all_workloads_pmc.md).  They hold for the kernel and
 # plan sources they were taken on; any other source reports null.
-TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "0a10e9155fd3842c"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160679589, "b1024_n1m_d768_bf16": 1573859155,
-                 "b4096_n4m_d512_f16": 6837671650, "b16384_n10m_d768_e4m3": 605971447785}
+TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/qs.hip",
+                   "paper_2502_06798_amd/csrc/simtopk.hip")
+TRAFFIC_SHA256 = "1bac6a0186bb2a87"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160888256, "b1024_n1m_d768_bf16": 1603740544,
+                 "b4096_n4m_d512_f16": 4433638208, "b16384_n10m_d768_e4m3": 518904240160}
 
 
 def log(*a):
