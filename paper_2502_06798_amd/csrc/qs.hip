@@ -33,16 +33,25 @@ __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, 
     float ss = 0.f;
     bool bad = false;
     const uint8_t* row = qry + r * row_bytes;
-    for (int64_t off = (int64_t)lane * 16; off < row_bytes; off += 64 * 16) {
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (r < b) {
-            v = *reinterpret_cast<const uint4*>(row + off);
-            sumsq16<DT>(v, ss, bad);
+    constexpr int U = 2;                                           // units per lane in flight
+    for (int64_t off0 = (int64_t)lane * 16; off0 < row_bytes; off0 += U * 64 * 16) {
+        uint4 v[U];
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            const int64_t off = off0 + i * 64 * 16;
+            v[i] = make_uint4(0u, 0u, 0u, 0u);
+            if (r < b && off < row_bytes) v[i] = *reinterpret_cast<const uint4*>(row + off);
         }
-        const int64_t u = (off >> 7) * 4 + ((off >> 4) & 3);     // unit within its half-row order
-        const int h = (int)((off >> 6) & 1);
-        const int64_t st = u / UPS, piece = u % UPS;
-        *reinterpret_cast<uint4*>(tp + (st * 64 + h * 32) * (UPS * 16) + piece * 16) = v;
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            const int64_t off = off0 + i * 64 * 16;
+            if (off >= row_bytes) continue;
+            if (r < b) sumsq16<DT>(v[i], ss, bad);
+            const int64_t u = (off >> 7) * 4 + ((off >> 4) & 3);  // unit within its half-row order
+            const int h = (int)((off >> 6) & 1);
+            const int64_t st = u / UPS, piece = u % UPS;
+            *reinterpret_cast<uint4*>(tp + (st * 64 + h * 32) * (UPS * 16) + piece * 16) = v[i];
+        }
     }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
