@@ -51,6 +51,7 @@ constexpr int Q2_FR = 8;                   // ring of per-group side data
 constexpr int Q2_KMAX = 32;                // largest k
 constexpr int Q2_LDS = 160 * 1024;         // LDS of a CU
 // s_waitcnt immediate: at most n vector-memory operations outstanding
+constexpr int Q2_PAIR_GROUPS = 8;          // groups of a split that bound the pair from both lists
 constexpr int q2_vmcnt(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
 
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes land
@@ -441,7 +442,7 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     }
     uint64_t wkey[MQ];   // the lane's k-th key (0 while it has fewer than k)
     int wp[MQ];          // its slot (lists in LDS)
-    float ps[MQ];        // the partner lane's k-th score (-inf while its list has empty slots)
+    float ps[MQ];        // a lower bound on the query's k-th best from the pair's lists (-inf until known)
 #pragma unroll
     for (int mq = 0; mq < MQ; ++mq) {
         wkey[mq] = 0;
@@ -663,13 +664,30 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                 if constexpr (LREG) wkey[mq] = q2_slot<KR>(lk[mq], k - 1);
             }
         }
-        // partner thresholds for the next group, and the global bound
+        // The pair's bound for the next group, and the global bound.  Besides
+        // either lane's k-th, with sorted lists: the smaller of one lane's m-th
+        // and the other's (k - m)-th best (m = ceil(k / 2)) has k pairs at or
+        // above it, which is far tighter while the lists are short (the first
+        // Q2_PAIR_GROUPS groups of a split; later it rarely beats the k-th and
+        // costs two slot selects per group).
 #pragma unroll
         for (int mq = 0; mq < MQ; ++mq) {
             const float own = q2_key_score(wkey[mq]);
-            ps[mq] = __shfl_xor(own, 32, 64);
-            const float best = __builtin_fmaxf(own, ps[mq]);
-            if (h == 0 && best > G[mq]) q2_atomic_max(gthr + q0w + mq * 32 + r32, q2_key(best));
+            float pair = __builtin_fmaxf(own, __shfl_xor(own, 32, 64));
+            if constexpr (LREG) {
+                if (k >= 2 && gi < Q2_PAIR_GROUPS) {               // uniform
+                    const int m1 = (k + 1) / 2, m2 = k - m1;
+                    const uint64_t a = q2_slot<KR>(lk[mq], m1 - 1), c = q2_slot<KR>(lk[mq], m2 - 1);
+                    const uint64_t pa = ((uint64_t)(uint32_t)__shfl_xor((int)(a >> 32), 32, 64) << 32) |
+                                        (uint32_t)__shfl_xor((int)(uint32_t)a, 32, 64);
+                    const uint64_t pc = ((uint64_t)(uint32_t)__shfl_xor((int)(c >> 32), 32, 64) << 32) |
+                                        (uint32_t)__shfl_xor((int)(uint32_t)c, 32, 64);
+                    const uint64_t t1 = a < pc ? a : pc, t2 = pa < c ? pa : c;
+                    pair = __builtin_fmaxf(pair, q2_key_score(t1 > t2 ? t1 : t2));
+                }
+            }
+            ps[mq] = pair;
+            if (h == 0 && pair > G[mq]) q2_atomic_max(gthr + q0w + mq * 32 + r32, q2_key(pair));
         }
     }
 
