@@ -155,10 +155,12 @@ def test_match_small(apc, orc, dtype, b, n, d, k):
     c.close()
 
 
-@pytest.mark.parametrize("dtype,b,n,d,k", [("f16", 2048, 40000, 768, 10), ("e4m3", 1024, 60000, 512, 12)])
+@pytest.mark.parametrize("dtype,b,n,d,k", [("f16", 2048, 40000, 768, 10), ("e4m3", 1024, 60000, 512, 12),
+                                            ("e4m3", 4096, 30000, 768, 32), ("f16", 4096, 20000, 512, 16)])
 def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
     """Enough query tiles that each split holds many groups: lists fill and
-    bounds tighten as the pass goes; a subset of rows is checked."""
+    bounds tighten as the pass goes; a subset of rows is checked.  The row
+    counts end in a partial group."""
     say(f"match (many groups per split) {dtype} b={b} n={n} d={d} k={k}")
     e, es = make_rows(n, d, dtype, 30 + n, clusters=max(1, n // 50))
     q, qs = make_rows(b, d, dtype, 40 + b, clusters=None)
