@@ -35,9 +35,9 @@ MALL_BYTES = 256 << 20
 # plan sources they were taken on; any other source reports null.
 TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/qs.hip",
                    "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "1bac6a0186bb2a87"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160888256, "b1024_n1m_d768_bf16": 1603740544,
-                 "b4096_n4m_d512_f16": 4433638208, "b16384_n10m_d768_e4m3": 518904240160}
+TRAFFIC_SHA256 = "2ae5a251f20c7199"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160864032, "b1024_n1m_d768_bf16": 1960373216,
+                 "b4096_n4m_d512_f16": 4432668736, "b16384_n10m_d768_e4m3": 490258889120}
 
 
 def log(*a):
