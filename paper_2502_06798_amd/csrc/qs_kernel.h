@@ -5,7 +5,8 @@
 // (its split).  Each wavefront keeps its MQ x 32 query rows in VGPRs for its
 // whole life, as the B operands of 32x32 MFMAs (lane l supplies query row
 // l % 32; half h = l / 32 supplies bytes [64h, 64h + 64) of every 128-byte
-// chunk of d).  Cache rows stream through an LDS ring in stages of EB x 32
+// chunk of d), loaded from a copy that the query preparation writes in the
+// order of these loads.  Cache rows stream through an LDS ring in stages of EB x 32
 // rows x 256 bytes, loaded straight from global memory into LDS (no VGPRs held
 // by loads in flight); a 16-byte unit of a row sits at unit ^ (row % 16), so
 // the A-operand reads (lane = row) are free of bank conflicts.  One barrier
@@ -24,13 +25,16 @@
 //    times entry factor, times f_q, clamped: both steps are monotone), and
 //    only if it reaches the filter threshold does the lane look further;
 //  * the filter threshold is the largest known lower bound on the query's
-//    k-th best score: the lane's own k-th, its partner lane's, and a
-//    per-query bound shared by all workgroups through atomic max (a published
-//    value is the k-th best score of some subset of the entries, so k entries
-//    score at least that much; ties with it are kept).  The shared bound is
-//    read as late as the LDS ring allows (with the next group's first stage),
-//    so that it includes what other workgroups found meanwhile;
-//  * the pairs that reach it go into the lane's list, one per pass.
+//    k-th best score: the pair's bound (either lane's k-th, and in a split's
+//    first groups the smaller of one lane's ceil(k/2)-th and the other's
+//    floor(k/2)-th) and a per-query bound shared by all workgroups through
+//    atomic max (a published value has k entries scoring at least that
+//    much; ties with it are kept).  The shared bound is read as late as the
+//    LDS ring allows (with the next group's first stage), so that it
+//    includes what other workgroups found meanwhile;
+//  * each pair's exact score is tested against it (one multiply and one
+//    compare), and the pairs that reach it go into the lane's list, one per
+//    pass.
 // At the end each lane's list is merged with its partner's, and the k best
 // are written as the split's partial list; k_topk_merge merges the splits.
 #pragma once
