@@ -456,49 +456,82 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 
     f32x16 acc[MQ][EB];      // written whole by each group's first MFMA step
 
-    // the stages of logical group gi (every wavefront, for the loads and barriers)
+    // the stages of logical group gi (every wavefront, for the loads and
+    // barriers).  The A fragments of step ss (all EB blocks) are read LA steps
+    // ahead of the MFMAs that use them; a scheduling barrier after each step
+    // keeps the compiler from regrouping the MFMAs by accumulator, which would
+    // wait out every read's latency and every MFMA's.  Within a group, the wait
+    // and barrier for the next stage come LA steps before the end of a stage,
+    // and the next stage's first LA reads go out while its last MFMAs run, so
+    // the matrix unit does not idle across the barrier.  Nothing is issued
+    // between the two points, so the wait counts are those of the next stage;
+    // the barrier comes after all of this stage's reads (it waits for them),
+    // so the next stage may refill this stage's slot.
+    constexpr int LA = SST < 3 ? SST : 2;
     auto run_group = [&](int gi) __attribute__((always_inline)) {
+        Step an[LA][EB];                                           // the next stage's first fragments
         static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
             constexpr int j = decltype(jc)::value;
+            constexpr bool early = j > 0;                          // wait, barrier, first reads done already
+            constexpr bool ahead = j + 1 < SPG;                    // do them for the next stage here
             const int t = gi * SPG + j;
-            if (t + NS - 2 < T) C::template wait_stage<j>();
-            else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
-            __syncthreads();
+            if constexpr (!early) {
+                if (t + NS - 2 < T) C::template wait_stage<j>();
+                else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
+                __syncthreads();
+            }
+            auto wait_next = [&]() __attribute__((always_inline)) {
+                if constexpr (ahead) {
+                    if (t + 1 + NS - 2 < T) C::template wait_stage<(ahead ? j + 1 : 0)>();
+                    else __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));
+                    __syncthreads();
+                }
+            };
             const uint8_t* sb = sm.e + (t % NS) * STAGE + r32 * Q2_SB;
-            // the A fragments of step ss (all EB blocks) are read LA steps ahead
-            // of the MFMAs that use them; a scheduling barrier after each step
-            // keeps the compiler from regrouping the MFMAs by accumulator, which
-            // would wait out every read's latency and every MFMA's
-            constexpr int LA = SST < 3 ? SST : 2;
+            const uint8_t* sbn = sm.e + ((t + 1) % NS) * STAGE + r32 * Q2_SB;
             Step a[SST][EB];
-            auto rd = [&](int ss) __attribute__((always_inline)) {
+            auto rd = [&](const uint8_t* base, int ss, Step (&dst)[EB]) __attribute__((always_inline)) {
                 const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
                 const int lu = cl * 8 + h * 4 + sp;                      // logical 16-byte unit
 #pragma unroll
                 for (int eb = 0; eb < EB; ++eb) {
-                    const uint8_t* rp = sb + eb * 32 * Q2_SB;
+                    const uint8_t* rp = base + eb * 32 * Q2_SB;
                     if constexpr (UPS == 1) {
-                        a[ss][eb] = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
+                        dst[eb] = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
                     } else {
                         const uint4 x0 = *reinterpret_cast<const uint4*>(rp + ((lu ^ (r32 & 15)) * 16));
                         const uint4 x1 = *reinterpret_cast<const uint4*>(rp + (((lu + 1) ^ (r32 & 15)) * 16));
-                        a[ss][eb] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
-                                         (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+                        dst[eb] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
+                                       (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
                     }
                 }
             };
             // the first reads go out before the stage loads are issued
             if (live) {
 #pragma unroll
-                for (int ss = 0; ss < LA; ++ss) rd(ss);
+                for (int ss = 0; ss < LA; ++ss) {
+                    if constexpr (early) {
+#pragma unroll
+                        for (int eb = 0; eb < EB; ++eb) a[ss][eb] = an[ss][eb];
+                    } else {
+                        rd(sb, ss, a[ss]);
+                    }
+                }
             }
             if (t + NS - 1 <= T)                                   // into the slot stage t - 1 used
                 issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
-            if (!live) return;
+            if (!live) {
+                wait_next();
+                return;
+            }
 
 #pragma unroll
             for (int ss = 0; ss < SST; ++ss) {
-                if (ss + LA < SST) rd(ss + LA);
+                if (ss + LA < SST) rd(sb, ss + LA, a[ss + LA]);
+                if constexpr (ahead) {
+                    if (ss == SST - LA) wait_next();
+                    if (ss >= SST - LA) rd(sbn, ss - (SST - LA), an[ss - (SST - LA)]);
+                }
 #pragma unroll
                 for (int eb = 0; eb < EB; ++eb)
 #pragma unroll
