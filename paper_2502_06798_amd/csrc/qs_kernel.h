@@ -586,9 +586,10 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         }
         if (gi == 0 && k <= 16) {
             // Seed for the first group (the lists are still empty): the 8 EB quads
-            // of a lane pair are disjoint, so with m = ceil(k/2), the smaller of
-            // one lane's m-th largest quad maximum and the other's (k-m)-th largest
-            // has k pairs at or above it.  Both pairings are valid; keep the larger.
+            // of a lane pair are disjoint, so the k-th largest of the pair's quad
+            // maxima has k pairs at or above it.  For k <= 4 EB it is found by
+            // merging the two lanes' sorted maxima; above that, the smaller of one
+            // lane's ceil(k/2)-th largest and the other's floor(k/2)-th serves.
             constexpr int NQ = 4 * EB;                             // quads per lane
 #pragma unroll
             for (int mq = 0; mq < MQ; ++mq) {
@@ -620,16 +621,38 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                                 qm[j] = sw ? a0 : a1;
                             }
                         }
-                const int m1 = (k + 1) / 2, m2 = k - m1;          // 1 <= m1 <= 8, 0 <= m2 <= 8
-                float a1 = qm[0], a2 = qm[0];
+                float seed;
+                if (k <= NQ) {                                     // uniform
+                    // own maxima (descending) against the partner's reversed form a
+                    // bitonic sequence whose larger elements are the NQ largest of
+                    // both; half-cleaners sort them
+                    float u[NQ];
 #pragma unroll
-                for (int p = 1; p < NQ; ++p) {
-                    a1 = p == m1 - 1 ? qm[p] : a1;
-                    a2 = p == m2 - 1 ? qm[p] : a2;
+                    for (int p = 0; p < NQ; ++p) u[p] = __builtin_fmaxf(qm[p], __shfl_xor(qm[NQ - 1 - p], 32, 64));
+#pragma unroll
+                    for (int stride = NQ / 2; stride > 0; stride /= 2)
+#pragma unroll
+                        for (int i = 0; i < NQ; ++i)
+                            if ((i & stride) == 0) {
+                                const float hi = __builtin_fmaxf(u[i], u[i + stride]);
+                                const float lo = __builtin_fminf(u[i], u[i + stride]);
+                                u[i] = hi;
+                                u[i + stride] = lo;
+                            }
+                    seed = u[0];
+#pragma unroll
+                    for (int p = 1; p < NQ; ++p) seed = p == k - 1 ? u[p] : seed;
+                } else {
+                    const int m1 = (k + 1) / 2, m2 = k - m1;      // 1 <= m1, m2 <= 8
+                    float a1 = qm[0], a2 = qm[0];
+#pragma unroll
+                    for (int p = 1; p < NQ; ++p) {
+                        a1 = p == m1 - 1 ? qm[p] : a1;
+                        a2 = p == m2 - 1 ? qm[p] : a2;
+                    }
+                    const float b1 = __shfl_xor(a1, 32, 64), b2 = __shfl_xor(a2, 32, 64);
+                    seed = __builtin_fmaxf(__builtin_fminf(a1, b2), __builtin_fminf(b1, a2));
                 }
-                if (m2 == 0) a2 = __builtin_huge_valf();
-                const float b1 = __shfl_xor(a1, 32, 64), b2 = __shfl_xor(a2, 32, 64);
-                const float seed = __builtin_fmaxf(__builtin_fminf(a1, b2), __builtin_fminf(b1, a2));
                 // as a score (NaN f_q leaves the seed at -inf through the comparison below)
                 const float ss = clamp1(seed * fq[mq]);
                 if (ss > ps[mq]) ps[mq] = ss;
