@@ -36,9 +36,9 @@ MALL_BYTES = 256 << 20
 # reports null.
 TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/qs.hip",
                    "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "057f6b21551e6a14"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160776416, "b1024_n1m_d768_bf16": 1572981376,
-                 "b4096_n4m_d512_f16": 4369138976, "b16384_n10m_d768_e4m3": 525489634624}
+TRAFFIC_SHA256 = "ac85d6eb1aa05c8a"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160748000, "b1024_n1m_d768_bf16": 1573725248,
+                 "b4096_n4m_d512_f16": 4369844000, "b16384_n10m_d768_e4m3": 518880819264}
 
 
 def log(*a):
