@@ -137,6 +137,67 @@ def copy_probe(mib, reps=5):
     print(json.dumps({"copy_probe_bytes": n, "reps": reps}), flush=True)
 
 
+SWEEP_CACHES = ("b1024_n1m_d768_bf16", "b16384_n10m_d768_e4m3")
+SWEEP_B = (1, 4, 16, 64, 128, 256)
+
+
+def sweep():
+    """Small batches against caches far larger than the 256 MB MALL, so every
+    match streams its cache from HBM: the similarity kernel's HBM rate against
+    the peak, per batch size."""
+    import numpy as np
+    import torch
+
+    import paper_2502_06798_amd as apc
+    from paper_2502_06798_amd import synth
+
+    apc.load()
+    for name in SWEEP_CACHES:
+        w = synth.BY_NAME[name]
+        log(f"generating {w.name}")
+        C = synth.centres(w, "cuda")
+        e, es = synth.entries(w, "cuda", C)
+        q, qs = synth.queries(w, "cuda", C)
+        del C
+        c = apc.apc_build_cache(e, es)
+        eb = {"f32": 4, "f16": 2, "bf16": 2, "e4m3": 1}[w.dtype]
+        for b in SWEEP_B:
+            qb = q[:b].contiguous()
+            qsb = None if qs is None else qs[:b].contiguous()
+            ts = torch.empty((b, w.k), dtype=torch.float32, device="cuda")
+            ti = torch.empty((b, w.k), dtype=torch.int32, device="cuda")
+            ws = apc.workspace_tensor(c, b, w.k)
+            reps = 40 if w.N * w.d * eb < 4 << 30 else 12
+            for _ in range(3):
+                apc.apc_match_batch(c, qb, qsb, w.k, ts, ti, ws)
+            torch.cuda.synchronize()
+            ev = HipEvents(reps)
+            for i in range(reps):
+                apc.apc_set_kernel_events(ev.pairs[i][0], ev.pairs[i][1])
+                apc.apc_match_batch(c, qb, qsb, w.k, ts, ti, ws)
+            torch.cuda.synchronize()
+            apc.apc_set_kernel_events(None, None)
+            kern = sorted(ev.elapsed_ms(i) for i in range(reps))
+            ev.close()
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                apc.apc_match_batch(c, qb, qsb, w.k, ts, ti, ws)
+            torch.cuda.synchronize()
+            match_ms = (time.perf_counter() - t0) / reps * 1e3
+            k50 = float(np.median(kern))
+            nbytes = w.N * w.d * eb + 4 * w.N + b * (w.d * eb + (4 if w.dtype == "e4m3" else 0)) + 8 * b * w.k
+            gbs = nbytes / (k50 * 1e-3) / 1e9
+            print(json.dumps({"sweep": w.name, "cache_bytes": w.N * w.d * eb, "B": b, "k": w.k,
+                              "sim_kernel_ms_p50": round(k50, 5),
+                              "sim_kernel_ms_p10": round(kern[len(kern) // 10], 5),
+                              "sim_kernel_ms_p90": round(kern[(9 * len(kern)) // 10], 5),
+                              "match_ms": round(match_ms, 5), "hbm_gbs": round(gbs, 1),
+                              "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}), flush=True)
+        c.close()
+        del e, es, q, qs
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +213,9 @@ def main():
                          "(measured slower on this stack: 0.131 vs 0.124 ms per step at b256)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain copy of this many MiB (HBM counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only run the small-batch streaming sweep: the b1024 (bf16) and b16384 (e4m3) "
+                         "caches against B = 1 ... 256 queries, one JSON line per point")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -167,6 +231,9 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib)
+        return
+    if args.sweep:
+        sweep()
         return
     apc.load()
     w = synth.BY_NAME[args.workload]
@@ -229,6 +296,32 @@ def main():
     wall = t1 - t0
     ms_per_step = wall / args.steps * 1e3
 
+    # spread of single steps (events around whole eager steps, a separate pass)
+    ns = min(args.steps, 50)
+    ev = HipEvents(ns)
+    ev.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    cur = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for i in range(ns):
+        ev.hip.hipEventRecord(ev.pairs[i][0], cur)
+        run(i)
+        ev.hip.hipEventRecord(ev.pairs[i][1], cur)
+    torch.cuda.synchronize()
+    step_ms = sorted(ev.elapsed_ms(i) for i in range(ns))
+    ev.close()
+    spread = {"p10": round(step_ms[ns // 10], 4), "p50": round(float(np.median(step_ms)), 4),
+              "p90": round(step_ms[(9 * ns) // 10], 4), "steps": ns}
+    # warm: one cache copy, left in the MALL between steps (only where it fits)
+    warm = None
+    if copies > 1:
+        for _ in range(5):
+            run(0)
+        torch.cuda.synchronize()
+        tw = time.perf_counter()
+        for _ in range(ns):
+            run(0)
+        torch.cuda.synchronize()
+        warm = round((time.perf_counter() - tw) / ns * 1e3, 4)
+
     flops = 2.0 * w.B * w.N * w.d
     nbytes = alg_bytes(w)
     ai = flops / nbytes
@@ -261,6 +354,8 @@ def main():
                    "cache_copies": copies, "launch": "hip_graph" if args.graph else "eager"},
         "sims_per_s": round(w.B * w.N / (kern_ms * 1e-3), 1),
         "sim_kernel_ms": round(kern_ms, 5),
+        "step_ms_spread": spread,
+        "warm_ms_per_step": warm,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
