@@ -76,7 +76,8 @@ typedef struct apc_cache apc_cache;
  *
  * The handle BORROWS emb, row_scale, latents and slot_of_entry: they must
  * stay alive and unchanged until apc_destroy_cache.  The library owns only
- * n float32 row factors (1 / norm) on the current device.  Waits for the
+ * the n float32 row factors (1 / norm; zero-padded past n to whole row
+ * groups) on the current device.  Waits for the
  * stream once and returns APC_E_NONFINITE / APC_E_ZERO_NORM / APC_E_ARG
  * (slot out of range) for bad data, with *out left NULL.
  */
