@@ -3,6 +3,9 @@
 TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
 benchmark's CPU-baseline leg, never by the library.  Shares no code with the
 HIP path.  Inputs are host numpy arrays holding the exact stored bytes.
+The Route-Plan (Eq. 1) and the placement that follows it are plain Python:
+the plan is scipy's LP solver on the transportation problem, the placement a
+loop over queries.
 """
 from __future__ import annotations
 
@@ -170,3 +173,123 @@ def gather(top1, out_level, out_inst, out_slot, slot_of_entry, n_entries, pool: 
 
 def max_threads() -> int:
     return int(lib().oracle_max_threads())
+
+
+# ---- Route-Plan (the K-to-K' Route Planner, Eq. 1) -------------------------
+# Reading of Eq. 1 (its constraint set is not printed): x[i, j] queries of
+# optimal level i are served at level j; a query is served at most once and
+# level j serves at most F[j]; serving level i at a level with more skipped
+# steps (K_j > K_i) degrades it by D = K_j - K_i, serving it at fewer skipped
+# steps costs nothing (Eq. 1 sums over K'_j > K_i only).  Queries that no
+# capacity can take stay unserved; the cost of leaving one unserved exceeds
+# any single move's degradation, so an optimum serves min(sum H, sum F).
+
+
+def _degradation_matrix(K):
+    Kf = np.concatenate([[0], np.asarray(K, dtype=np.int64)])
+    n = Kf.size
+    return np.array([[max(0, int(Kf[j] - Kf[i])) for j in range(n)] for i in range(n)], dtype=np.int64)
+
+
+def route_plan(H, F, K):
+    """Optimal integer plan x ((L+1) x (L+1), int64), its degradation and the
+    number served, by scipy's LP solver (HiGHS dual simplex) on the
+    transportation problem above.  H, F: per-level demand and capacity
+    (levels 0..L); K: skipped steps of levels 1..L (level 0 skips none).
+    A basic optimal solution of a transportation problem with integral
+    supplies and capacities is integral; the function checks that it is."""
+    from scipy.optimize import linprog
+    H = np.asarray(H, dtype=np.int64)
+    F = np.asarray(F, dtype=np.int64)
+    n = H.size
+    cost = _degradation_matrix(K).astype(np.float64)
+    unserved = float(cost.max() + 1.0)
+    c = np.concatenate([cost.ravel(), np.full(n, unserved)])
+    A_eq = np.zeros((n, n * n + n))                  # row i: sum_j x[i, j] + unserved_i = H[i]
+    for i in range(n):
+        A_eq[i, i * n:(i + 1) * n] = 1.0
+        A_eq[i, n * n + i] = 1.0
+    A_ub = np.zeros((n, n * n + n))                  # column j: sum_i x[i, j] <= F[j]
+    for j in range(n):
+        A_ub[j, j:n * n:n] = 1.0
+    res = linprog(c, A_ub=A_ub, b_ub=F.astype(np.float64), A_eq=A_eq, b_eq=H.astype(np.float64),
+                  bounds=(0, None), method="highs-ds")
+    if res.status != 0:
+        raise RuntimeError(f"route_plan: LP failed: {res.message}")
+    x = res.x[:n * n].reshape(n, n)
+    xi = np.rint(x).astype(np.int64)
+    if np.abs(x - xi).max() > 1e-6:
+        raise RuntimeError("route_plan: the LP vertex is not integral")
+    d, served = plan_cost(xi, K)
+    return xi, d, served
+
+
+def plan_cost(x, K):
+    """(degradation, number served) of a plan x under the reading above."""
+    x = np.asarray(x, dtype=np.int64)
+    return int((x * _degradation_matrix(K)).sum()), int(x.sum())
+
+
+def preference(lam: int, L: int):
+    """Redirection order of a query of optimal level lam: its own level, then
+    the levels below it, closest first, then the levels above it, closest
+    first (the Approach's K-to-K' redirection)."""
+    return [lam] + list(range(lam - 1, -1, -1)) + list(range(lam + 1, L + 1))
+
+
+def assign_routed(level, L: int, x, inst_level, inst_cap, inst_queue=None):
+    """Placement that follows a route plan x (negative entries count as 0).
+    The queries of optimal level i, in index order, take the levels of their
+    preference list in that order, x[i, j] of them for level j; queries past
+    sum_j x[i, j] get none.  A level then admits the queries routed to it by
+    (position of the level in the query's preference list, query index) while
+    it has places; admission rank t lands on the level's instances ordered by
+    (queue desc, index asc), each filled to its capacity, slots from 0.
+    Given the flow that the rounds placement (assign) realises, this returns
+    exactly that placement.  Returns (out_level, out_inst, out_slot,
+    inst_fill), int32."""
+    level = np.asarray(level, dtype=np.int64)
+    x = np.maximum(np.asarray(x, dtype=np.int64), 0)
+    b, n_inst = level.size, len(inst_level)
+    seen = [0] * (L + 1)
+    want = np.full(b, -1, dtype=np.int64)
+    rnd = np.full(b, -1, dtype=np.int64)
+    for q in range(b):
+        i = int(level[q])
+        r = seen[i]
+        seen[i] += 1
+        acc = 0
+        for pos, j in enumerate(preference(i, L)):
+            acc += int(x[i, j])
+            if r < acc:
+                want[q], rnd[q] = j, pos
+                break
+    cap = [0] * (L + 1)
+    for a in range(n_inst):
+        cap[inst_level[a]] += int(inst_cap[a])
+    queue = [0] * n_inst if inst_queue is None else list(inst_queue)
+    order = sorted(range(n_inst), key=lambda a: (inst_level[a], -queue[a], a))
+    used = [0] * (L + 1)
+    out_level = np.full(b, -1, dtype=np.int32)
+    out_inst = np.full(b, -1, dtype=np.int32)
+    out_slot = np.full(b, -1, dtype=np.int32)
+    fill = np.zeros(n_inst, dtype=np.int32)
+    for r in range(L + 1):
+        for q in range(b):
+            if rnd[q] != r:
+                continue
+            j = int(want[q])
+            t = used[j]
+            if t >= cap[j]:
+                continue
+            used[j] += 1
+            out_level[q] = j
+            for a in order:
+                if inst_level[a] != j:
+                    continue
+                if t < inst_cap[a]:
+                    out_inst[q], out_slot[q] = a, t
+                    fill[a] += 1
+                    break
+                t -= inst_cap[a]
+    return out_level, out_inst, out_slot, fill
