@@ -213,6 +213,9 @@ def main():
                          "(measured slower on this stack: 0.131 vs 0.124 ms per step at b256)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain copy of this many MiB (HBM counter calibration)")
+    ap.add_argument("--route", choices=("rounds", "planned"), default="rounds",
+                    help="placement: preference-order rounds (apc_assign) or the batch's optimal "
+                         "Route-Plan applied as quotas (apc_assign_planned)")
     ap.add_argument("--sweep", action="store_true",
                     help="only run the small-batch streaming sweep: the b1024 (bf16) and b16384 (e4m3) "
                          "caches against B = 1 ... 256 queries, one JSON line per point")
@@ -251,7 +254,8 @@ def main():
     copies = args.copies or (1 if cache_bytes > MALL_BYTES else min(8, -(-(5 * MALL_BYTES) // cache_bytes)))
     embs = [e] + [e.clone() for _ in range(copies - 1)]
     caches = [apc.apc_build_cache(x, es, pool, soe) for x in embs]
-    step = apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes)
+    step = apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes,
+                         route=args.route)
     torch.cuda.synchronize()
 
     def run(i):
@@ -310,6 +314,16 @@ def main():
     ev.close()
     spread = {"p10": round(step_ms[ns // 10], 4), "p50": round(float(np.median(step_ms)), 4),
               "p90": round(step_ms[(9 * ns) // 10], 4), "steps": ns}
+    # the placement kernel alone (on the last step's scores)
+    ev = HipEvents(ns)
+    ev.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    for i in range(ns):
+        ev.hip.hipEventRecord(ev.pairs[i][0], cur)
+        step.assign()
+        ev.hip.hipEventRecord(ev.pairs[i][1], cur)
+    torch.cuda.synchronize()
+    assign_ms = float(np.median([ev.elapsed_ms(i) for i in range(ns)]))
+    ev.close()
     # warm: one cache copy, left in the MALL between steps (only where it fits)
     warm = None
     if copies > 1:
@@ -351,11 +365,13 @@ def main():
         "data": "synthetic (seeded clustered Gaussian embeddings standing in for prompt embeddings)",
         "config": {"workload": w.name, "B": w.B, "N": w.N, "d": w.d, "k": w.k, "levels": w.L,
                    "instances": w.n_inst, "capacity": w.cap, "latent_bytes": w.latent_bytes,
-                   "cache_copies": copies, "launch": "hip_graph" if args.graph else "eager"},
+                   "cache_copies": copies, "launch": "hip_graph" if args.graph else "eager",
+                   "route": args.route},
         "sims_per_s": round(w.B * w.N / (kern_ms * 1e-3), 1),
         "sim_kernel_ms": round(kern_ms, 5),
         "step_ms_spread": spread,
         "warm_ms_per_step": warm,
+        "assign_ms": round(assign_ms, 5),
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -55,6 +55,7 @@ typedef enum {
 #define APC_MAX_K 64          /* largest neighbour count per query */
 #define APC_MAX_LEVELS 32     /* largest number of skip levels L */
 #define APC_MAX_INST 256      /* largest number of model instances */
+#define APC_MAX_ROUTED_BATCH 16384  /* largest batch of apc_assign_routed / apc_assign_planned */
 
 /* opaque, immutable after build */
 typedef struct apc_cache apc_cache;
@@ -154,6 +155,71 @@ apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L,
                       const int32_t* inst_queue /* host, nullable */, int32_t* opt_level,
                       int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
                       int32_t* inst_fill, void* stream);
+
+/*
+ * Route-Plan (Eq. 1; the K-to-K' Route Planner of the Resource Controller):
+ * an optimal integer plan X for serving per-level demand H with per-level
+ * places F.  Host only: no GPU, no stream.
+ *
+ * Reading of Eq. 1 (its constraints are not printed): X[i][j] >= 0 queries of
+ * optimal level i are served at level j, sum_j X[i][j] <= H[i] and
+ * sum_i X[i][j] <= F[j]; min(sum H, sum F) queries are served (an unserved
+ * query costs more than any move), and among such plans the degradation
+ *   D = sum_{j > i} X[i][j] * (K_j - K_i)      (K_0 = 0)
+ * is minimal; moves to fewer skipped steps (j < i) cost nothing.  Excess
+ * demand is left unserved from the lowest levels up.  Of the optimal plans
+ * the one returned serves each level's own queries first and moves the rest
+ * in first-in-first-out order along the levels; it is deterministic.
+ *
+ * L, K        0 <= L <= APC_MAX_LEVELS; K (host) L skip counts of levels
+ *             1..L, > 0 and strictly increasing (NULL when L = 0).
+ * H, F        (host) L+1 demands and places per level, >= 0, each sum <= 2^31-1.
+ * X           (host, out) (L+1) x (L+1) int32, row-major: X[i * (L+1) + j].
+ * degradation (host, out, nullable) D of X.
+ * Errors: APC_E_TABLE for L or K out of range, APC_E_ARG for NULL or negative
+ * inputs or sums past 2^31-1; X is not written then.
+ */
+apc_status apc_route_plan(int32_t L, const int32_t* K, const int32_t* H, const int32_t* F, int32_t* X,
+                          int64_t* degradation);
+
+/*
+ * Placement that follows a route plan (the K-to-K' Router applying the
+ * Route-Plan as per-(K, K') quotas instead of the rounds of apc_assign).
+ * Arguments, outputs and errors as for apc_assign, plus:
+ *
+ * plan        (device, in) (L+1) x (L+1) int32 quotas X, row-major; negative
+ *             entries count as 0.
+ * b           <= APC_MAX_ROUTED_BATCH (else APC_E_ARG).
+ * Placement: the queries of optimal level i, in index order, take the levels
+ *             of their preference list [i, i-1, .., 0, i+1, .., L] in that
+ *             order, X[i][j] of them for level j; queries past sum_j X[i][j]
+ *             get out_level = -1.  A level admits the queries routed to it by
+ *             (position of the level in the query's preference list, query
+ *             index) while it has places (later ones get -1); admission rank
+ *             t goes to the level's instances ordered by (queue desc, index
+ *             asc), each up to its capacity, slots from 0.  Given the flow
+ *             X[i][j] that apc_assign realises, the result equals apc_assign's.
+ */
+apc_status apc_assign_routed(const float* top_score, int32_t ld, int32_t b, int32_t L,
+                             const float* theta /* host */, const int32_t* K /* host */, int32_t n_inst,
+                             const int32_t* inst_level /* host */, const int32_t* inst_cap /* host */,
+                             const int32_t* inst_queue /* host, nullable */, const int32_t* plan /* device */,
+                             int32_t* opt_level, int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
+                             int32_t* inst_fill, void* stream);
+
+/*
+ * apc_assign_routed with the plan built on the device, in the same kernel,
+ * from the batch's own level histogram H (H[l] = #{q : opt_level[q] = l}),
+ * the places per level F (sum of inst_cap over the level's instances) and K:
+ * the plan apc_route_plan returns for (L, K, H, F), written to plan (device,
+ * out, (L+1) x (L+1) int32).  One launch, no host round trip.
+ */
+apc_status apc_assign_planned(const float* top_score, int32_t ld, int32_t b, int32_t L,
+                              const float* theta /* host */, const int32_t* K /* host */, int32_t n_inst,
+                              const int32_t* inst_level /* host */, const int32_t* inst_cap /* host */,
+                              const int32_t* inst_queue /* host, nullable */, int32_t* plan /* device */,
+                              int32_t* opt_level, int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
+                              int32_t* inst_fill, void* stream);
 
 /*
  * Latent gather (the cached intermediate state a placed prompt starts from):

@@ -62,6 +62,12 @@ def load() -> ctypes.CDLL:
     L.apc_match_batch.restype = st
     L.apc_assign.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.apc_assign.restype = st
+    L.apc_route_plan.argtypes = [i32, vp, vp, vp, vp, ctypes.POINTER(i64)]
+    L.apc_route_plan.restype = st
+    L.apc_assign_routed.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.apc_assign_routed.restype = st
+    L.apc_assign_planned.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.apc_assign_planned.restype = st
     L.apc_gather_latents.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, vp, vp, vp]
     L.apc_gather_latents.restype = st
     L.apc_set_kernel_events.argtypes = [vp, vp]
@@ -201,6 +207,48 @@ def apc_assign(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float],
     _check(load().apc_assign(_ptr(top_score), ld, b, th.size, _hp(th), _hp(Kh), il.size, _hp(il),
                              _hp(ic), _hp(iq), _ptr(opt_level), _ptr(out_level), _ptr(out_inst),
                              _ptr(out_slot), _ptr(inst_fill), _stream(stream)))
+
+
+def apc_route_plan(K: Sequence[int], H: Sequence[int], F: Sequence[int]):
+    """Host-only Route-Plan: returns (X as an (L+1) x (L+1) int32 array, degradation)."""
+    Kh = _host(K, np.int32)
+    Hh = _host(H, np.int32)
+    Fh = _host(F, np.int32)
+    L = Kh.size
+    if Hh.size != L + 1 or Fh.size != L + 1:
+        raise ValueError("apc_route_plan: H and F need len(K) + 1 entries")
+    X = np.zeros((L + 1, L + 1), dtype=np.int32)
+    d = ctypes.c_int64(0)
+    _check(load().apc_route_plan(L, _hp(Kh), _hp(Hh), _hp(Fh), X.ctypes.data, ctypes.byref(d)))
+    return X, int(d.value)
+
+
+def _assign_plan(fn, top_score, ld, b, theta, K, inst_level, inst_cap, inst_queue, plan, opt_level,
+                 out_level, out_inst, out_slot, inst_fill, stream):
+    th = _host(theta, np.float32)
+    Kh = _host(K, np.int32)
+    il = _host(inst_level, np.int32)
+    ic = _host(inst_cap, np.int32)
+    iq = _host(inst_queue, np.int32)
+    _check(fn(_ptr(top_score), ld, b, th.size, _hp(th), _hp(Kh), il.size, _hp(il), _hp(ic), _hp(iq),
+              _ptr(plan), _ptr(opt_level), _ptr(out_level), _ptr(out_inst), _ptr(out_slot),
+              _ptr(inst_fill), _stream(stream)))
+
+
+def apc_assign_routed(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float], K: Sequence[int],
+                      inst_level: Sequence[int], inst_cap: Sequence[int], inst_queue: Optional[Sequence[int]],
+                      plan: torch.Tensor, opt_level: torch.Tensor, out_level: torch.Tensor,
+                      out_inst: torch.Tensor, out_slot: torch.Tensor, inst_fill: torch.Tensor, stream=None):
+    _assign_plan(load().apc_assign_routed, top_score, ld, b, theta, K, inst_level, inst_cap, inst_queue,
+                 plan, opt_level, out_level, out_inst, out_slot, inst_fill, stream)
+
+
+def apc_assign_planned(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float], K: Sequence[int],
+                       inst_level: Sequence[int], inst_cap: Sequence[int], inst_queue: Optional[Sequence[int]],
+                       plan: torch.Tensor, opt_level: torch.Tensor, out_level: torch.Tensor,
+                       out_inst: torch.Tensor, out_slot: torch.Tensor, inst_fill: torch.Tensor, stream=None):
+    _assign_plan(load().apc_assign_planned, top_score, ld, b, theta, K, inst_level, inst_cap, inst_queue,
+                 plan, opt_level, out_level, out_inst, out_slot, inst_fill, stream)
 
 
 def apc_gather_latents(c: Cache, top_idx: torch.Tensor, ld: int, b: int, out_level: torch.Tensor,

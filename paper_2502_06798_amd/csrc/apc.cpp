@@ -12,6 +12,7 @@
 #include <string>
 
 #include "apc_internal.h"
+#include "route_plan.h"
 
 struct apc_cache {
     apc_dtype dt;
@@ -249,40 +250,49 @@ apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_sca
     return ok();
 }
 
-apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
-                      const int32_t* K, int32_t n_inst, const int32_t* inst_level, const int32_t* inst_cap,
-                      const int32_t* inst_queue, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
-                      int32_t* out_slot, int32_t* inst_fill, void* stream)
+namespace {
+
+// Checks the level and instance tables shared by the assignment entry points
+// and builds the device table (levels, instances ordered by (level, queue
+// desc, index asc), places per level).
+apc_status build_assign_table(const char* who, const float* top_score, int32_t ld, int32_t b, int32_t L,
+                              const float* theta, const int32_t* K, int32_t n_inst, const int32_t* inst_level,
+                              const int32_t* inst_cap, const int32_t* inst_queue, const int32_t* opt_level,
+                              const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                              const int32_t* inst_fill, apc::AssignTable& t)
 {
-    if (b < 0 || ld < 1) return fail(APC_E_ARG, "apc_assign: need b >= 0 and ld >= 1");
-    if (L < 0 || L > APC_MAX_LEVELS) return fail(APC_E_TABLE, "apc_assign: need 0 <= L <= %d", APC_MAX_LEVELS);
-    if (L > 0 && (!theta || !K)) return fail(APC_E_TABLE, "apc_assign: theta/K are NULL");
+    if (b < 0 || ld < 1) return fail(APC_E_ARG, "%s: need b >= 0 and ld >= 1", who);
+    if (L < 0 || L > APC_MAX_LEVELS) return fail(APC_E_TABLE, "%s: need 0 <= L <= %d", who, APC_MAX_LEVELS);
+    if (L > 0 && (!theta || !K)) return fail(APC_E_TABLE, "%s: theta/K are NULL", who);
     for (int l = 0; l < L; ++l) {
-        if (!std::isfinite(theta[l])) return fail(APC_E_TABLE, "apc_assign: theta[%d] is not finite", l);
-        if (K[l] <= 0) return fail(APC_E_TABLE, "apc_assign: K[%d] must be > 0", l);
+        if (!std::isfinite(theta[l])) return fail(APC_E_TABLE, "%s: theta[%d] is not finite", who, l);
+        if (K[l] <= 0) return fail(APC_E_TABLE, "%s: K[%d] must be > 0", who, l);
         if (l > 0 && !(theta[l] > theta[l - 1]))
-            return fail(APC_E_TABLE, "apc_assign: thresholds must be strictly increasing");
-        if (l > 0 && !(K[l] > K[l - 1])) return fail(APC_E_TABLE, "apc_assign: K must be strictly increasing");
+            return fail(APC_E_TABLE, "%s: thresholds must be strictly increasing", who);
+        if (l > 0 && !(K[l] > K[l - 1])) return fail(APC_E_TABLE, "%s: K must be strictly increasing", who);
     }
     if (n_inst < 0 || n_inst > APC_MAX_INST)
-        return fail(APC_E_TABLE, "apc_assign: need 0 <= n_inst <= %d", APC_MAX_INST);
-    if (n_inst > 0 && (!inst_level || !inst_cap)) return fail(APC_E_TABLE, "apc_assign: instance table is NULL");
+        return fail(APC_E_TABLE, "%s: need 0 <= n_inst <= %d", who, APC_MAX_INST);
+    if (n_inst > 0 && (!inst_level || !inst_cap)) return fail(APC_E_TABLE, "%s: instance table is NULL", who);
     int64_t total = 0;
     for (int i = 0; i < n_inst; ++i) {
         if (inst_level[i] < 0 || inst_level[i] > L)
-            return fail(APC_E_TABLE, "apc_assign: inst_level[%d] = %d not in 0..%d", i, inst_level[i], L);
-        if (inst_cap[i] < 0) return fail(APC_E_TABLE, "apc_assign: inst_cap[%d] < 0", i);
+            return fail(APC_E_TABLE, "%s: inst_level[%d] = %d not in 0..%d", who, i, inst_level[i], L);
+        if (inst_cap[i] < 0) return fail(APC_E_TABLE, "%s: inst_cap[%d] < 0", who, i);
         total += inst_cap[i];
     }
-    if (total > INT32_MAX) return fail(APC_E_TABLE, "apc_assign: total capacity exceeds 2^31 - 1");
+    if (total > INT32_MAX) return fail(APC_E_TABLE, "%s: total capacity exceeds 2^31 - 1", who);
     if (b > 0 && (!top_score || !opt_level || !out_level || !out_inst || !out_slot))
-        return fail(APC_E_ARG, "apc_assign: NULL device buffer");
-    if (n_inst > 0 && !inst_fill) return fail(APC_E_ARG, "apc_assign: inst_fill is NULL");
+        return fail(APC_E_ARG, "%s: NULL device buffer", who);
+    if (n_inst > 0 && !inst_fill) return fail(APC_E_ARG, "%s: inst_fill is NULL", who);
 
-    apc::AssignTable t{};
+    t = apc::AssignTable{};
     t.L = L;
     t.n_inst = n_inst;
-    for (int l = 0; l < L; ++l) t.theta[l] = theta[l];
+    for (int l = 0; l < L; ++l) {
+        t.theta[l] = theta[l];
+        t.K[l + 1] = K[l];
+    }
     int order[APC_MAX_INST];
     for (int i = 0; i < n_inst; ++i) order[i] = i;
     std::stable_sort(order, order + n_inst, [&](int a, int c) {
@@ -305,11 +315,91 @@ apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L, 
         t.level_cap[p] = (int32_t)cum;
     }
     t.level_first[L + 1] = j;
+    return APC_OK;
+}
+
+}  // namespace
+
+apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
+                      const int32_t* K, int32_t n_inst, const int32_t* inst_level, const int32_t* inst_cap,
+                      const int32_t* inst_queue, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                      int32_t* out_slot, int32_t* inst_fill, void* stream)
+{
+    apc::AssignTable t;
+    apc_status st = build_assign_table("apc_assign", top_score, ld, b, L, theta, K, n_inst, inst_level, inst_cap,
+                                       inst_queue, opt_level, out_level, out_inst, out_slot, inst_fill, t);
+    if (st != APC_OK) return st;
     if (b == 0 && n_inst == 0) return ok();
     hipError_t e = apc::launch_assign(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot,
                                       inst_fill, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "apc_assign launch");
     return ok();
+}
+
+apc_status apc_route_plan(int32_t L, const int32_t* K, const int32_t* H, const int32_t* F, int32_t* X,
+                          int64_t* degradation)
+{
+    if (L < 0 || L > APC_MAX_LEVELS) return fail(APC_E_TABLE, "apc_route_plan: need 0 <= L <= %d", APC_MAX_LEVELS);
+    if ((L > 0 && !K) || !H || !F || !X) return fail(APC_E_ARG, "apc_route_plan: NULL argument");
+    for (int l = 0; l < L; ++l) {
+        if (K[l] <= 0) return fail(APC_E_TABLE, "apc_route_plan: K[%d] must be > 0", l);
+        if (l > 0 && !(K[l] > K[l - 1])) return fail(APC_E_TABLE, "apc_route_plan: K must be strictly increasing");
+    }
+    int64_t sh = 0, sf = 0;
+    for (int i = 0; i <= L; ++i) {
+        if (H[i] < 0 || F[i] < 0) return fail(APC_E_ARG, "apc_route_plan: H[%d] or F[%d] < 0", i, i);
+        sh += H[i];
+        sf += F[i];
+    }
+    if (sh > INT32_MAX || sf > INT32_MAX) return fail(APC_E_ARG, "apc_route_plan: sums exceed 2^31 - 1");
+    apc::plan_route_host(L, H, F, X);
+    if (degradation) {
+        int64_t d = 0;
+        for (int i = 0; i <= L; ++i)
+            for (int j = i + 1; j <= L; ++j)
+                d += (int64_t)X[i * (L + 1) + j] * ((int64_t)K[j - 1] - (i > 0 ? K[i - 1] : 0));
+        *degradation = d;
+    }
+    return ok();
+}
+
+static apc_status assign_with_plan(const char* who, bool planned, const float* top_score, int32_t ld, int32_t b,
+                                   int32_t L, const float* theta, const int32_t* K, int32_t n_inst,
+                                   const int32_t* inst_level, const int32_t* inst_cap, const int32_t* inst_queue,
+                                   int32_t* plan, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                                   int32_t* out_slot, int32_t* inst_fill, void* stream)
+{
+    apc::AssignTable t;
+    apc_status st = build_assign_table(who, top_score, ld, b, L, theta, K, n_inst, inst_level, inst_cap,
+                                       inst_queue, opt_level, out_level, out_inst, out_slot, inst_fill, t);
+    if (st != APC_OK) return st;
+    if (b > APC_MAX_ROUTED_BATCH) return fail(APC_E_ARG, "%s: b = %d exceeds %d", who, b, APC_MAX_ROUTED_BATCH);
+    if (!plan) return fail(APC_E_ARG, "%s: plan is NULL", who);
+    hipError_t e = apc::launch_assign_plan(t, planned, top_score, ld, b, plan, opt_level, out_level, out_inst,
+                                           out_slot, inst_fill, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+apc_status apc_assign_routed(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
+                             const int32_t* K, int32_t n_inst, const int32_t* inst_level, const int32_t* inst_cap,
+                             const int32_t* inst_queue, const int32_t* plan, int32_t* opt_level,
+                             int32_t* out_level, int32_t* out_inst, int32_t* out_slot, int32_t* inst_fill,
+                             void* stream)
+{
+    return assign_with_plan("apc_assign_routed", false, top_score, ld, b, L, theta, K, n_inst, inst_level,
+                            inst_cap, inst_queue, const_cast<int32_t*>(plan), opt_level, out_level, out_inst,
+                            out_slot, inst_fill, stream);
+}
+
+apc_status apc_assign_planned(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
+                              const int32_t* K, int32_t n_inst, const int32_t* inst_level, const int32_t* inst_cap,
+                              const int32_t* inst_queue, int32_t* plan, int32_t* opt_level, int32_t* out_level,
+                              int32_t* out_inst, int32_t* out_slot, int32_t* inst_fill, void* stream)
+{
+    return assign_with_plan("apc_assign_planned", true, top_score, ld, b, L, theta, K, n_inst, inst_level,
+                            inst_cap, inst_queue, plan, opt_level, out_level, out_inst, out_slot, inst_fill,
+                            stream);
 }
 
 apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,

@@ -91,6 +91,7 @@ struct AssignTable {
     int32_t L;
     int32_t n_inst;
     float theta[APC_MAX_LEVELS];
+    int32_t K[APC_MAX_LEVELS + 1];               // skipped steps per level, K[0] = 0
     int32_t level_cap[APC_MAX_LEVELS + 1];       // places per level
     int32_t level_first[APC_MAX_LEVELS + 2];     // first ordered instance of each level
     int16_t ord_inst[APC_MAX_INST];              // instances by (level, queue desc, index asc)
@@ -101,6 +102,12 @@ struct AssignTable {
 hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t ld, int32_t b,
                          int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
                          int32_t* out_slot, int32_t* inst_fill, hipStream_t s);
+
+// Placement that follows a route plan (planned: computed in the kernel from
+// the batch's level histogram and written to plan; else read from plan).
+hipError_t launch_assign_plan(const AssignTable& t, bool planned, const float* top_score, int32_t ld, int32_t b,
+                              int32_t* plan, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                              int32_t* out_slot, int32_t* inst_fill, hipStream_t s);
 
 // ---- gather ----------------------------------------------------------------
 hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,

@@ -13,6 +13,7 @@
 // level's instances ordered by (queue desc, index asc), each filled up to
 // its capacity.
 #include "apc_internal.h"
+#include "route_plan.h"
 
 namespace apc {
 namespace {
@@ -239,6 +240,207 @@ __global__ __launch_bounds__(NTB) void k_assign_reg(const AssignTable targ, cons
         }
 }
 
+// Placement that follows a route plan x (queries of optimal level i served
+// at level j).  Same block shape and per-thread query ownership as
+// k_assign_reg.  Pass 1 ranks every query among the queries of its own level
+// in index order (per-level ballots, per-wave totals, chunks in order), which
+// also yields the batch's level histogram H.  With PLANNED the block then
+// builds the optimal plan from H, the places per level and K (one thread per
+// level, then one per plan entry) and writes it out; otherwise it reads the
+// caller's plan (negative entries count as 0).  A query of level i with rank
+// s takes the first level j of its preference list [i, i-1, .., 0, i+1, .., L]
+// where s falls below the running sum of x[i][.]; the position of j in that
+// list is the query's round.  Pass 2 admits, round by round and in index
+// order within a round, every query to its level while the level has places
+// (the same rank computation as the rounds placement, without retries).
+template <int QPT, int NTB, bool PLANNED>
+__global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, const float* __restrict__ top_score,
+                                                     int32_t ld, int32_t b, int32_t* __restrict__ plan,
+                                                     int32_t* __restrict__ opt_level,
+                                                     int32_t* __restrict__ out_level,
+                                                     int32_t* __restrict__ out_inst,
+                                                     int32_t* __restrict__ out_slot,
+                                                     int32_t* __restrict__ inst_fill)
+{
+    constexpr int NT = NTB, NWAVE = NTB / 64, NL = APC_MAX_LEVELS + 1;
+    __shared__ int cnt[2][NL];
+    __shared__ int wcnt[NWAVE][NL];
+    __shared__ int xs[NL * NL];
+    __shared__ PlanWork w;
+    __shared__ unsigned long long rounds;                    // bit r: some query is admitted in round r
+    __shared__ AssignTable t;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float best[QPT];
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        const int q = c * NT + tid;
+        best[c] = q < b ? top_score[(int64_t)q * ld] : 0.f;
+    }
+    table_to_lds<NT>(targ, t, tid);
+    const int L = t.L, n = L + 1;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int nchunk = (b + NT - 1) / NT;
+    int lam[QPT], rs[QPT], dr[QPT], rk[QPT];
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        const int q = c * NT + tid;
+        lam[c] = -1;
+        rk[c] = -1;
+        if (q < b) {
+            lam[c] = 0;
+            for (int l = 0; l < L; ++l) lam[c] += best[c] >= t.theta[l];
+        }
+    }
+    if (tid <= L) cnt[0][tid] = 0;
+    if (tid == 0) rounds = 0ull;
+    int cur = 0;
+    // Pass 1: rank among the queries of the same level; the histogram.
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        if (c < nchunk) {                                     // uniform
+            int pre = 0;
+            for (int p = 0; p <= L; ++p) {
+                const uint64_t m = __ballot(lam[c] == p);
+                if (lam[c] == p) pre = __popcll(m & lt_mask);
+                if (lane == 0) wcnt[wave][p] = __popcll(m);
+            }
+            __syncthreads();
+            if (lam[c] >= 0) {
+                int r = cnt[cur][lam[c]] + pre;
+#pragma unroll
+                for (int ww = 0; ww < NWAVE; ++ww) r += ww < wave ? wcnt[ww][lam[c]] : 0;
+                rs[c] = r;
+            }
+            if (tid <= L) {
+                int tot = cnt[cur][tid];
+#pragma unroll
+                for (int ww = 0; ww < NWAVE; ++ww) tot += wcnt[ww][tid];
+                cnt[cur ^ 1][tid] = tot;
+            }
+            __syncthreads();
+            cur ^= 1;
+        }
+    }
+    __syncthreads();                                          // b = 0: cnt[0] and rounds initialised
+    // The plan.
+    if (PLANNED) {
+        if (tid <= L) plan_level_own(L, cnt[cur], t.level_cap, tid, w);
+        __syncthreads();
+        if (tid < L) plan_level_flow(L, tid, w);
+        if (tid == L) w.n[L] = 0;
+        __syncthreads();
+        if (tid <= L) plan_level_intervals(L, tid, w);
+        __syncthreads();
+        for (int e = tid; e < n * n; e += NT) {
+            const int v = plan_entry(e / n, e % n, w);
+            xs[e] = v;
+            plan[e] = v;
+        }
+    } else {
+        for (int e = tid; e < n * n; e += NT) {
+            const int v = plan[e];
+            xs[e] = v < 0 ? 0 : v;
+        }
+    }
+    __syncthreads();
+    // Destination and round of every query.
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        dr[c] = -1;
+        if (c < nchunk && lam[c] >= 0) {
+            const int i = lam[c];
+            int64_t acc = 0;
+            for (int pos = 0; pos <= L; ++pos) {
+                const int j = pos == 0 ? i : (pos <= i ? i - pos : pos);
+                acc += xs[i * n + j];
+                if (rs[c] < acc) {
+                    dr[c] = j | (pos << 8);
+                    atomicOr(&rounds, 1ull << pos);
+                    break;
+                }
+            }
+        }
+    }
+    if (tid <= L) cnt[cur][tid] = 0;                          // now the places taken per level
+    __syncthreads();
+    const unsigned long long rmask = rounds;
+    // Pass 2: admission by (round, index).
+    for (int r = 0; r <= L; ++r) {
+        if (!((rmask >> r) & 1ull)) continue;                 // uniform
+#pragma unroll
+        for (int c = 0; c < QPT; ++c) {
+            if (c < nchunk) {                                 // uniform
+                const int want = (dr[c] >= 0 && (dr[c] >> 8) == r) ? (dr[c] & 0xff) : -1;
+                int pre = 0;
+                for (int p = 0; p <= L; ++p) {
+                    const uint64_t m = __ballot(want == p);
+                    if (want == p) pre = __popcll(m & lt_mask);
+                    if (lane == 0) wcnt[wave][p] = __popcll(m);
+                }
+                __syncthreads();
+                if (want >= 0) {
+                    int rank = cnt[cur][want] + pre;
+#pragma unroll
+                    for (int ww = 0; ww < NWAVE; ++ww) rank += ww < wave ? wcnt[ww][want] : 0;
+                    if (rank < t.level_cap[want]) rk[c] = rank;
+                }
+                if (tid <= L) {
+                    int tot = cnt[cur][tid];
+#pragma unroll
+                    for (int ww = 0; ww < NWAVE; ++ww) tot += wcnt[ww][tid];
+                    const int cap = t.level_cap[tid];
+                    cnt[cur ^ 1][tid] = tot < cap ? tot : cap;
+                }
+                __syncthreads();
+                cur ^= 1;
+            }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        const int q = c * NT + tid;
+        if (q >= b) continue;
+        const int p = rk[c] >= 0 ? (dr[c] & 0xff) : -1;
+        int inst = -1, slot = -1;
+        if (p >= 0) {
+            for (int j = t.level_first[p]; j < t.level_first[p + 1]; ++j)
+                if (rk[c] < t.ord_cum[j] + t.ord_cap[j]) {
+                    inst = t.ord_inst[j];
+                    slot = rk[c] - t.ord_cum[j];
+                    break;
+                }
+        }
+        opt_level[q] = lam[c];
+        out_level[q] = p;
+        out_inst[q] = inst;
+        out_slot[q] = slot;
+    }
+    for (int p = 0; p <= L; ++p)
+        for (int j = t.level_first[p] + tid; j < t.level_first[p + 1]; j += NT) {
+            int f = cnt[cur][p] - t.ord_cum[j];
+            f = f < 0 ? 0 : (f > t.ord_cap[j] ? t.ord_cap[j] : f);
+            inst_fill[t.ord_inst[j]] = f;
+        }
+}
+
+template <bool PLANNED>
+hipError_t launch_plan_t(const AssignTable& t, const float* top_score, int32_t ld, int32_t b, int32_t* plan,
+                         int32_t* opt_level, int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
+                         int32_t* inst_fill, hipStream_t s)
+{
+    if (b <= 256)
+        k_assign_plan<1, 256, PLANNED><<<1, 256, 0, s>>>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= NT)
+        k_assign_plan<1, NT, PLANNED><<<1, NT, 0, s>>>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= 4 * NT)
+        k_assign_plan<4, NT, PLANNED><<<1, NT, 0, s>>>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else if (b <= 16 * NT)
+        k_assign_plan<16, NT, PLANNED><<<1, NT, 0, s>>>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t ld, int32_t b,
@@ -256,6 +458,15 @@ hipError_t launch_assign(const AssignTable& t, const float* top_score, int32_t l
     else
         k_assign<<<1, NT, 0, s>>>(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill);
     return hipGetLastError();
+}
+
+hipError_t launch_assign_plan(const AssignTable& t, bool planned, const float* top_score, int32_t ld, int32_t b,
+                              int32_t* plan, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
+                              int32_t* out_slot, int32_t* inst_fill, hipStream_t s)
+{
+    static_assert(16 * NT == APC_MAX_ROUTED_BATCH, "largest routed batch");
+    return planned ? launch_plan_t<true>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill, s)
+                   : launch_plan_t<false>(t, top_score, ld, b, plan, opt_level, out_level, out_inst, out_slot, inst_fill, s);
 }
 
 }  // namespace apc

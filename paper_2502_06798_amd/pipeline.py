@@ -17,8 +17,10 @@ class MatchStep:
     def __init__(self, cache: B.Cache, b: int, k: int, theta: Sequence[float], K: Sequence[int],
                  inst_level: Sequence[int], inst_cap: Sequence[int],
                  inst_queue: Optional[Sequence[int]] = None, slots_per_inst: Optional[int] = None,
-                 latent_bytes: int = 0, device="cuda"):
-        self.cache, self.b, self.k = cache, b, k
+                 latent_bytes: int = 0, device="cuda", route: str = "rounds"):
+        if route not in ("rounds", "planned"):
+            raise ValueError("route is 'rounds' (preference-order rounds) or 'planned' (Route-Plan quotas)")
+        self.cache, self.b, self.k, self.route = cache, b, k, route
         self.theta = np.ascontiguousarray(theta, dtype=np.float32)
         self.K = np.ascontiguousarray(K, dtype=np.int32)
         self.inst_level = np.ascontiguousarray(inst_level, dtype=np.int32)
@@ -36,6 +38,8 @@ class MatchStep:
         self.out_slot = torch.empty(b, **i32)
         self.inst_fill = torch.empty(max(self.n_inst, 1), **i32)
         self.hit = torch.empty(b, **i32)
+        n_lv = self.K.size + 1
+        self.plan = torch.empty(n_lv * n_lv, **i32) if route == "planned" else None
         self.latent_bytes = latent_bytes
         self.batch = (torch.empty((self.n_inst * self.spi, latent_bytes), dtype=torch.uint8, device=device)
                       if latent_bytes else None)
@@ -44,6 +48,11 @@ class MatchStep:
         B.apc_match_batch(self.cache, q, q_scale, self.k, self.top_score, self.top_idx, self.ws, stream)
 
     def assign(self, stream=None):
+        if self.route == "planned":
+            B.apc_assign_planned(self.top_score, self.k, self.b, self.theta, self.K, self.inst_level,
+                                 self.inst_cap, self.inst_queue, self.plan, self.opt_level, self.out_level,
+                                 self.out_inst, self.out_slot, self.inst_fill, stream)
+            return
         B.apc_assign(self.top_score, self.k, self.b, self.theta, self.K, self.inst_level, self.inst_cap,
                      self.inst_queue, self.opt_level, self.out_level, self.out_inst, self.out_slot,
                      self.inst_fill, stream)
