@@ -240,6 +240,10 @@ __global__ __launch_bounds__(NTB) void k_assign_reg(const AssignTable targ, cons
         }
 }
 
+// Position of level j in the preference list of level i, and its inverse.
+__device__ inline int pref_pos(int i, int j) { return j == i ? 0 : (j < i ? i - j : j); }
+__device__ inline int pref_at(int i, int pos) { return pos == 0 ? i : (pos <= i ? i - pos : pos); }
+
 // Placement that follows a route plan x (queries of optimal level i served
 // at level j).  Same block shape and per-thread query ownership as
 // k_assign_reg.  Pass 1 ranks every query among the queries of its own level
@@ -249,10 +253,13 @@ __global__ __launch_bounds__(NTB) void k_assign_reg(const AssignTable targ, cons
 // level, then one per plan entry) and writes it out; otherwise it reads the
 // caller's plan (negative entries count as 0).  A query of level i with rank
 // s takes the first level j of its preference list [i, i-1, .., 0, i+1, .., L]
-// where s falls below the running sum of x[i][.]; the position of j in that
-// list is the query's round.  Pass 2 admits, round by round and in index
-// order within a round, every query to its level while the level has places
-// (the same rank computation as the rounds placement, without retries).
+// where s falls below the running sum of x[i][.]; the position pos of j in
+// that list is its round.  A level admits in (round, index) order while it
+// has places, so a query's admission rank is the number of queries routed to
+// j in earlier rounds (from the realised flow) plus its rank inside group
+// (j, pos).  Only group (j, j) mixes queries of several levels; pass 2 ranks
+// its members with one ballot per such level, the others are ranked by their
+// offset in their level's quota.
 template <int QPT, int NTB, bool PLANNED>
 __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, const float* __restrict__ top_score,
                                                      int32_t ld, int32_t b, int32_t* __restrict__ plan,
@@ -266,8 +273,12 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
     __shared__ int cnt[2][NL];
     __shared__ int wcnt[NWAVE][NL];
     __shared__ int xs[NL * NL];
+    __shared__ int fs[NL * NL];                              // realised flow, level i -> level j
+    __shared__ int gb[NL * NL];                              // [j * n + pos]: places before group (j, pos)
+    __shared__ int used[NL];                                 // places taken per level
+    __shared__ int cnt2[2][NL];
     __shared__ PlanWork w;
-    __shared__ unsigned long long rounds;                    // bit r: some query is admitted in round r
+    __shared__ unsigned long long multi;                     // bit j: group (j, j) has members
     __shared__ AssignTable t;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float best[QPT];
@@ -280,7 +291,7 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
     const int L = t.L, n = L + 1;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const int nchunk = (b + NT - 1) / NT;
-    int lam[QPT], rs[QPT], dr[QPT], rk[QPT];
+    int lam[QPT], rs[QPT], dr[QPT], ik[QPT], rk[QPT];
 #pragma unroll
     for (int c = 0; c < QPT; ++c) {
         const int q = c * NT + tid;
@@ -292,7 +303,6 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
         }
     }
     if (tid <= L) cnt[0][tid] = 0;
-    if (tid == 0) rounds = 0ull;
     int cur = 0;
     // Pass 1: rank among the queries of the same level; the histogram.
 #pragma unroll
@@ -321,7 +331,7 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
             cur ^= 1;
         }
     }
-    __syncthreads();                                          // b = 0: cnt[0] and rounds initialised
+    __syncthreads();                                          // b = 0: cnt[0] initialised
     // The plan.
     if (PLANNED) {
         if (tid <= L) plan_level_own(L, cnt[cur], t.level_cap, tid, w);
@@ -343,57 +353,98 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
         }
     }
     __syncthreads();
-    // Destination and round of every query.
+    // Realised flow: how many of level i's queries the plan sends to level j
+    // (the row's quotas taken in preference order until the level runs out).
+    const int* H = cnt[cur];
+    for (int e = tid; e < n * n; e += NT) {
+        const int i = e / n, j = e - i * n, pj = pref_pos(i, j);
+        int64_t before = 0;
+        for (int pos = 0; pos < pj; ++pos) before += xs[i * n + pref_at(i, pos)];
+        int64_t f = (int64_t)H[i] - before;
+        f = f < 0 ? 0 : (f > xs[e] ? xs[e] : f);
+        fs[e] = (int)f;
+    }
+    if (tid == 0) multi = 0ull;
+    __syncthreads();
+    // Places at level j taken before group (j, pos), i.e. by earlier positions.
+    for (int e = tid; e < n * n; e += NT) {
+        const int j = e / n, pos = e - j * n;
+        int base = 0;
+        for (int i = 0; i <= L; ++i) base += pref_pos(i, j) < pos ? fs[i * n + j] : 0;
+        gb[e] = base;
+    }
+    if (tid <= L) {
+        int tot = 0;
+        for (int i = 0; i <= L; ++i) tot += fs[i * n + tid];
+        used[tid] = tot < t.level_cap[tid] ? tot : t.level_cap[tid];
+        cnt2[0][tid] = 0;
+    }
+    // Destination, position and rank inside its group (j, pos).  A group with
+    // pos != j holds queries of one level i only (i = j + pos, or i = j for
+    // pos = 0), in index order, so the rank is the offset in i's quota.  Group
+    // (j, j) gathers the moves up from every level below j (and the move down
+    // from level 2j): ranked by ballots below.
 #pragma unroll
     for (int c = 0; c < QPT; ++c) {
         dr[c] = -1;
+        ik[c] = -1;
         if (c < nchunk && lam[c] >= 0) {
             const int i = lam[c];
             int64_t acc = 0;
             for (int pos = 0; pos <= L; ++pos) {
-                const int j = pos == 0 ? i : (pos <= i ? i - pos : pos);
-                acc += xs[i * n + j];
+                const int j = pref_at(i, pos);
+                const int x = xs[i * n + j];
+                acc += x;
                 if (rs[c] < acc) {
                     dr[c] = j | (pos << 8);
-                    atomicOr(&rounds, 1ull << pos);
+                    if (pos == j && j > 0) atomicOr(&multi, 1ull << j);
+                    else ik[c] = rs[c] - (int)(acc - x);
                     break;
                 }
             }
         }
     }
-    if (tid <= L) cnt[cur][tid] = 0;                          // now the places taken per level
     __syncthreads();
-    const unsigned long long rmask = rounds;
-    // Pass 2: admission by (round, index).
-    for (int r = 0; r <= L; ++r) {
-        if (!((rmask >> r) & 1ull)) continue;                 // uniform
+    const unsigned long long mm = multi;
+    cur = 0;
+    if (mm) {                                                 // uniform
 #pragma unroll
         for (int c = 0; c < QPT; ++c) {
             if (c < nchunk) {                                 // uniform
-                const int want = (dr[c] >= 0 && (dr[c] >> 8) == r) ? (dr[c] & 0xff) : -1;
+                const int g = (dr[c] >= 0 && ik[c] < 0) ? (dr[c] & 0xff) : -1;
                 int pre = 0;
-                for (int p = 0; p <= L; ++p) {
-                    const uint64_t m = __ballot(want == p);
-                    if (want == p) pre = __popcll(m & lt_mask);
-                    if (lane == 0) wcnt[wave][p] = __popcll(m);
+                for (unsigned long long bits = mm; bits; bits &= bits - 1) {
+                    const int j = __builtin_ctzll(bits);
+                    const uint64_t m = __ballot(g == j);
+                    if (g == j) pre = __popcll(m & lt_mask);
+                    if (lane == 0) wcnt[wave][j] = __popcll(m);
                 }
                 __syncthreads();
-                if (want >= 0) {
-                    int rank = cnt[cur][want] + pre;
+                if (g >= 0) {
+                    int r = cnt2[cur][g] + pre;
 #pragma unroll
-                    for (int ww = 0; ww < NWAVE; ++ww) rank += ww < wave ? wcnt[ww][want] : 0;
-                    if (rank < t.level_cap[want]) rk[c] = rank;
+                    for (int ww = 0; ww < NWAVE; ++ww) r += ww < wave ? wcnt[ww][g] : 0;
+                    ik[c] = r;
                 }
-                if (tid <= L) {
-                    int tot = cnt[cur][tid];
+                if (tid <= L && ((mm >> tid) & 1ull)) {
+                    int tot = cnt2[cur][tid];
 #pragma unroll
                     for (int ww = 0; ww < NWAVE; ++ww) tot += wcnt[ww][tid];
-                    const int cap = t.level_cap[tid];
-                    cnt[cur ^ 1][tid] = tot < cap ? tot : cap;
+                    cnt2[cur ^ 1][tid] = tot;
                 }
                 __syncthreads();
                 cur ^= 1;
             }
+        }
+    }
+    // Admission rank at the level: earlier groups, then the rank in the group.
+#pragma unroll
+    for (int c = 0; c < QPT; ++c) {
+        rk[c] = -1;
+        if (dr[c] >= 0) {
+            const int j = dr[c] & 0xff, pos = dr[c] >> 8;
+            const int rank = gb[j * n + pos] + ik[c];
+            if (rank < t.level_cap[j]) rk[c] = rank;
         }
     }
 #pragma unroll
@@ -417,7 +468,7 @@ __global__ __launch_bounds__(NTB) void k_assign_plan(const AssignTable targ, con
     }
     for (int p = 0; p <= L; ++p)
         for (int j = t.level_first[p] + tid; j < t.level_first[p + 1]; j += NT) {
-            int f = cnt[cur][p] - t.ord_cum[j];
+            int f = used[p] - t.ord_cum[j];
             f = f < 0 ? 0 : (f > t.ord_cap[j] ? t.ord_cap[j] : f);
             inst_fill[t.ord_inst[j]] = f;
         }
