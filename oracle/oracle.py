@@ -293,3 +293,42 @@ def assign_routed(level, L: int, x, inst_level, inst_cap, inst_queue=None):
                     break
                 t -= inst_cap[a]
     return out_level, out_inst, out_slot, fill
+
+
+# ---- Resident-aware fallback and the level histogram -----------------------
+# A query can only start from a cached state that is resident.  Reading: when
+# its nearest entry's latent is not resident, the query falls back to the best
+# of its k neighbours whose latent is; the level then follows that
+# neighbour's score.  With none resident it gets no score (NaN, level 0).
+
+def resident_best(top_score, top_idx, k: int, slot_of_entry, n_slots: int):
+    """For each query row of the (b, >= k) top lists: (score, entry) of the
+    first of its k neighbours with a resident latent (slot_of_entry[e] >= 0
+    and < n_slots; slot_of_entry None means entry e lives in slot e), else
+    (NaN, -1).  The lists are ordered best first, so the first is the best."""
+    top_score = np.asarray(top_score, dtype=np.float32)
+    top_idx = np.asarray(top_idx, dtype=np.int64)
+    b = top_idx.shape[0]
+    out_s = np.full(b, np.nan, dtype=np.float32)
+    out_i = np.full(b, -1, dtype=np.int32)
+    for q in range(b):
+        for j in range(k):
+            e = int(top_idx[q, j])
+            if e < 0:
+                continue
+            slot = e if slot_of_entry is None else int(slot_of_entry[e])
+            if 0 <= slot < n_slots:
+                out_s[q], out_i[q] = top_score[q, j], e
+                break
+    return out_s, out_i
+
+
+def level_histogram(level, L: int):
+    """H[l] = number of queries whose optimal level is l, l = 0..L (values
+    outside 0..L are not counted); the per-batch demand of the Optimal-K
+    Predictor and of the Route-Plan."""
+    H = np.zeros(L + 1, dtype=np.int64)
+    for v in np.asarray(level).tolist():
+        if 0 <= v <= L:
+            H[v] += 1
+    return H
