@@ -216,6 +216,9 @@ def main():
     ap.add_argument("--route", choices=("rounds", "planned"), default="rounds",
                     help="placement: preference-order rounds (apc_assign) or the batch's optimal "
                          "Route-Plan applied as quotas (apc_assign_planned)")
+    ap.add_argument("--resident-fallback", action="store_true",
+                    help="level and latent follow the best neighbour whose latent is resident "
+                         "(apc_resident_best) instead of the top-1")
     ap.add_argument("--sweep", action="store_true",
                     help="only run the small-batch streaming sweep: the b1024 (bf16) and b16384 (e4m3) "
                          "caches against B = 1 ... 256 queries, one JSON line per point")
@@ -255,7 +258,7 @@ def main():
     embs = [e] + [e.clone() for _ in range(copies - 1)]
     caches = [apc.apc_build_cache(x, es, pool, soe) for x in embs]
     step = apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes,
-                         route=args.route)
+                         route=args.route, resident_fallback=args.resident_fallback)
     torch.cuda.synchronize()
 
     def run(i):
@@ -314,6 +317,8 @@ def main():
     ev.close()
     spread = {"p10": round(step_ms[ns // 10], 4), "p50": round(float(np.median(step_ms)), 4),
               "p90": round(step_ms[(9 * ns) // 10], 4), "steps": ns}
+    # share of the batch that starts from a gathered latent (last step)
+    hit_rate = round(float(step.hit.float().mean().item()), 4) if step.batch is not None else None
     # the placement kernel alone (on the last step's scores)
     ev = HipEvents(ns)
     ev.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
@@ -366,12 +371,13 @@ def main():
         "config": {"workload": w.name, "B": w.B, "N": w.N, "d": w.d, "k": w.k, "levels": w.L,
                    "instances": w.n_inst, "capacity": w.cap, "latent_bytes": w.latent_bytes,
                    "cache_copies": copies, "launch": "hip_graph" if args.graph else "eager",
-                   "route": args.route},
+                   "route": args.route, "resident_fallback": args.resident_fallback},
         "sims_per_s": round(w.B * w.N / (kern_ms * 1e-3), 1),
         "sim_kernel_ms": round(kern_ms, 5),
         "step_ms_spread": spread,
         "warm_ms_per_step": warm,
         "assign_ms": round(assign_ms, 5),
+        "latent_hit_rate": hit_rate,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

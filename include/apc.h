@@ -222,6 +222,33 @@ apc_status apc_assign_planned(const float* top_score, int32_t ld, int32_t b, int
                               int32_t* inst_fill, void* stream);
 
 /*
+ * Resident-aware fallback (a query starts from a cached state only if that
+ * state is resident, Introduction and Approach): for each query, the first of
+ * its k neighbours top_idx[q * ld + 0..k-1] (ordered best first, as
+ * apc_match_batch writes them) whose entry has a resident latent in cache c
+ * (slot_of_entry[e] in 0..n_slots-1; every entry e < n_slots when the cache
+ * was built without slot_of_entry).  out_score[q] / out_idx[q] = that
+ * neighbour's score and entry, NaN / -1 when none of the k is resident (or
+ * the entries are -1).  Passing out_score, out_idx with ld = 1 to apc_assign
+ * and apc_gather_latents places each query at the level its best reusable
+ * neighbour supports (level 0 when none) and gathers that latent.
+ *
+ * 1 <= k <= min(ld, APC_MAX_K); the cache must hold latents (n_slots > 0).
+ * Errors: APC_E_ARG for bad sizes, NULL buffers or a cache without latents.
+ */
+apc_status apc_resident_best(const apc_cache* c, const float* top_score, const int32_t* top_idx, int32_t ld,
+                             int32_t k, int32_t b, float* out_score, int32_t* out_idx, void* stream);
+
+/*
+ * Level histogram of a batch (the demand H_K per optimal K that the
+ * Optimal-K Predictor of the Resource Controller forecasts, and the Route-Plan
+ * takes): hist[l] = #{q < b : level[q] == l}, l = 0..L; other values are not
+ * counted.  level and hist are device buffers (b and L + 1 int32);
+ * 0 <= L <= APC_MAX_LEVELS.  Errors: APC_E_ARG.
+ */
+apc_status apc_level_histogram(const int32_t* level, int32_t b, int32_t L, int32_t* hist, void* stream);
+
+/*
  * Latent gather (the cached intermediate state a placed prompt starts from):
  * for each query with out_level > 0 whose top-1 entry top_idx[q * ld] has a
  * resident latent, copy it to batch_latents[(out_inst * slots_per_inst +

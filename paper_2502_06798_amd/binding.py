@@ -68,6 +68,10 @@ def load() -> ctypes.CDLL:
     L.apc_assign_routed.restype = st
     L.apc_assign_planned.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.apc_assign_planned.restype = st
+    L.apc_resident_best.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp, vp]
+    L.apc_resident_best.restype = st
+    L.apc_level_histogram.argtypes = [vp, i32, i32, vp, vp]
+    L.apc_level_histogram.restype = st
     L.apc_gather_latents.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, vp, vp, vp]
     L.apc_gather_latents.restype = st
     L.apc_set_kernel_events.argtypes = [vp, vp]
@@ -249,6 +253,16 @@ def apc_assign_planned(top_score: torch.Tensor, ld: int, b: int, theta: Sequence
                        out_inst: torch.Tensor, out_slot: torch.Tensor, inst_fill: torch.Tensor, stream=None):
     _assign_plan(load().apc_assign_planned, top_score, ld, b, theta, K, inst_level, inst_cap, inst_queue,
                  plan, opt_level, out_level, out_inst, out_slot, inst_fill, stream)
+
+
+def apc_resident_best(c: Cache, top_score: torch.Tensor, top_idx: torch.Tensor, ld: int, k: int, b: int,
+                      out_score: torch.Tensor, out_idx: torch.Tensor, stream=None):
+    _check(load().apc_resident_best(c.handle, _ptr(top_score), _ptr(top_idx), ld, k, b, _ptr(out_score),
+                                    _ptr(out_idx), _stream(stream)))
+
+
+def apc_level_histogram(level: torch.Tensor, b: int, L: int, hist: torch.Tensor, stream=None):
+    _check(load().apc_level_histogram(_ptr(level), b, L, _ptr(hist), _stream(stream)))
 
 
 def apc_gather_latents(c: Cache, top_idx: torch.Tensor, ld: int, b: int, out_level: torch.Tensor,

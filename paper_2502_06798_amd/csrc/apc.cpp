@@ -402,6 +402,32 @@ apc_status apc_assign_planned(const float* top_score, int32_t ld, int32_t b, int
                             stream);
 }
 
+apc_status apc_resident_best(const apc_cache* c, const float* top_score, const int32_t* top_idx, int32_t ld,
+                             int32_t k, int32_t b, float* out_score, int32_t* out_idx, void* stream)
+{
+    if (!c) return fail(APC_E_ARG, "apc_resident_best: NULL cache");
+    if (c->n_slots == 0) return fail(APC_E_ARG, "apc_resident_best: the cache has no latents");
+    if (b < 0 || k < 1 || k > APC_MAX_K || ld < k)
+        return fail(APC_E_ARG, "apc_resident_best: need b >= 0 and 1 <= k <= min(ld, %d)", APC_MAX_K);
+    if (b == 0) return ok();
+    if (!top_score || !top_idx || !out_score || !out_idx)
+        return fail(APC_E_ARG, "apc_resident_best: NULL device buffer");
+    hipError_t e = apc::launch_resident_best(c->slot_of_entry, c->n, c->n_slots, top_score, top_idx, ld, k, b,
+                                             out_score, out_idx, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_resident_best launch");
+    return ok();
+}
+
+apc_status apc_level_histogram(const int32_t* level, int32_t b, int32_t L, int32_t* hist, void* stream)
+{
+    if (b < 0 || L < 0 || L > APC_MAX_LEVELS)
+        return fail(APC_E_ARG, "apc_level_histogram: need b >= 0 and 0 <= L <= %d", APC_MAX_LEVELS);
+    if ((b > 0 && !level) || !hist) return fail(APC_E_ARG, "apc_level_histogram: NULL device buffer");
+    hipError_t e = apc::launch_level_histogram(level, b, L, hist, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_level_histogram launch");
+    return ok();
+}
+
 apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
                               const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
                               int32_t n_inst, int32_t slots_per_inst, void* batch_latents, int32_t* hit,

@@ -109,6 +109,12 @@ hipError_t launch_assign_plan(const AssignTable& t, bool planned, const float* t
                               int32_t* plan, int32_t* opt_level, int32_t* out_level, int32_t* out_inst,
                               int32_t* out_slot, int32_t* inst_fill, hipStream_t s);
 
+// ---- resident-aware fallback, level histogram ----
+hipError_t launch_resident_best(const int32_t* slot_of_entry, int64_t n_entries, int64_t n_slots,
+                                const float* top_score, const int32_t* top_idx, int32_t ld, int32_t k, int32_t b,
+                                float* out_score, int32_t* out_idx, hipStream_t s);
+hipError_t launch_level_histogram(const int32_t* level, int32_t b, int32_t L, int32_t* hist, hipStream_t s);
+
 // ---- gather ----------------------------------------------------------------
 hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,
                          const int32_t* slot_of_entry, const int32_t* top_idx, int32_t ld, int32_t b,

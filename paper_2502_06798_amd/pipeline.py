@@ -17,10 +17,13 @@ class MatchStep:
     def __init__(self, cache: B.Cache, b: int, k: int, theta: Sequence[float], K: Sequence[int],
                  inst_level: Sequence[int], inst_cap: Sequence[int],
                  inst_queue: Optional[Sequence[int]] = None, slots_per_inst: Optional[int] = None,
-                 latent_bytes: int = 0, device="cuda", route: str = "rounds"):
+                 latent_bytes: int = 0, device="cuda", route: str = "rounds", resident_fallback: bool = False):
         if route not in ("rounds", "planned"):
             raise ValueError("route is 'rounds' (preference-order rounds) or 'planned' (Route-Plan quotas)")
         self.cache, self.b, self.k, self.route = cache, b, k, route
+        # with resident_fallback, the level and the latent follow the best
+        # neighbour whose latent is resident (apc_resident_best), not the top-1
+        self.resident_fallback = resident_fallback
         self.theta = np.ascontiguousarray(theta, dtype=np.float32)
         self.K = np.ascontiguousarray(K, dtype=np.int32)
         self.inst_level = np.ascontiguousarray(inst_level, dtype=np.int32)
@@ -38,6 +41,8 @@ class MatchStep:
         self.out_slot = torch.empty(b, **i32)
         self.inst_fill = torch.empty(max(self.n_inst, 1), **i32)
         self.hit = torch.empty(b, **i32)
+        self.res_score = torch.empty(b, dtype=torch.float32, device=device) if resident_fallback else None
+        self.res_idx = torch.empty(b, **i32) if resident_fallback else None
         n_lv = self.K.size + 1
         self.plan = torch.empty(n_lv * n_lv, **i32) if route == "planned" else None
         self.latent_bytes = latent_bytes
@@ -46,21 +51,32 @@ class MatchStep:
 
     def match(self, q: torch.Tensor, q_scale: Optional[torch.Tensor] = None, stream=None):
         B.apc_match_batch(self.cache, q, q_scale, self.k, self.top_score, self.top_idx, self.ws, stream)
+        if self.resident_fallback:
+            B.apc_resident_best(self.cache, self.top_score, self.top_idx, self.k, self.k, self.b,
+                                self.res_score, self.res_idx, stream)
+
+    def _best(self):
+        """(scores, entries, row stride) that the level and the gather follow."""
+        if self.resident_fallback:
+            return self.res_score, self.res_idx, 1
+        return self.top_score, self.top_idx, self.k
 
     def assign(self, stream=None):
+        sc, _, ld = self._best()
         if self.route == "planned":
-            B.apc_assign_planned(self.top_score, self.k, self.b, self.theta, self.K, self.inst_level,
+            B.apc_assign_planned(sc, ld, self.b, self.theta, self.K, self.inst_level,
                                  self.inst_cap, self.inst_queue, self.plan, self.opt_level, self.out_level,
                                  self.out_inst, self.out_slot, self.inst_fill, stream)
             return
-        B.apc_assign(self.top_score, self.k, self.b, self.theta, self.K, self.inst_level, self.inst_cap,
+        B.apc_assign(sc, ld, self.b, self.theta, self.K, self.inst_level, self.inst_cap,
                      self.inst_queue, self.opt_level, self.out_level, self.out_inst, self.out_slot,
                      self.inst_fill, stream)
 
     def gather(self, stream=None):
         if self.batch is None:
             return
-        B.apc_gather_latents(self.cache, self.top_idx, self.k, self.b, self.out_level, self.out_inst,
+        _, ix, ld = self._best()
+        B.apc_gather_latents(self.cache, ix, ld, self.b, self.out_level, self.out_inst,
                              self.out_slot, self.n_inst, self.spi, self.batch, self.hit, stream)
 
     def run(self, q: torch.Tensor, q_scale: Optional[torch.Tensor] = None, stream=None):

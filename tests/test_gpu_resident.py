@@ -1,0 +1,125 @@
+"""GPU parity of the resident-aware fallback and the level histogram.
+
+apc_resident_best is compared bit for bit with the oracle on the same seeded
+top lists (ordered, with ties, invalid entries, every residency from none to
+all, k from 1 to 64, ragged batches), and end to end after apc_match_batch
+on rows whose neighbour lists agree with the oracle's exact top-k.
+apc_level_histogram is compared bit for bit with the oracle's counts.
+"""
+import numpy as np
+import pytest
+import torch
+
+from tests._util import stored_np
+from tests.gpu_check import TOL, say
+from tests.test_gpu_parity import make_rows
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def apc():
+    import paper_2502_06798_amd as apc
+    apc.load()
+    assert torch.cuda.is_available()
+    return apc
+
+
+def _lists(rng, b, ld, n):
+    s = np.round(rng.uniform(-1, 1, (b, ld)), 2).astype(np.float32)
+    idx = np.stack([rng.choice(n, ld, replace=False) for _ in range(b)]).astype(np.int32)
+    for q in range(b):
+        o = np.lexsort((idx[q], -s[q].astype(np.float64)))
+        s[q], idx[q] = s[q][o], idx[q][o]
+    idx[rng.random((b, ld)) < 0.02] = -1
+    return s, idx
+
+
+def _cache(apc, n, n_slots, frac, rng, with_map=True):
+    e, _ = make_rows(n, 64, "f16", 5)
+    pool = torch.zeros((n_slots, 16), dtype=torch.uint8, device="cuda")
+    if not with_map:
+        return apc.apc_build_cache(e, None, pool, None), None
+    soe = np.full(n, -1, np.int32)
+    hot = rng.choice(n, int(round(frac * n)), replace=False)
+    soe[hot] = rng.integers(0, n_slots, hot.size)
+    return apc.apc_build_cache(e, None, pool, torch.from_numpy(soe).cuda()), soe
+
+
+@pytest.mark.parametrize("b,ld,k,frac", [(1, 1, 1, 1.0), (5, 10, 10, 0.2), (1000, 12, 10, 0.05),
+                                         (3001, 32, 32, 0.01), (4096, 64, 64, 0.03), (700, 40, 33, 0.0),
+                                         (16384, 32, 32, 0.02)])
+def test_resident_best_bit_exact(apc, orc, b, ld, k, frac):
+    say(f"resident_best b={b} ld={ld} k={k} frac={frac}")
+    rng = np.random.default_rng(b + k)
+    n, n_slots = 4000, 300
+    c, soe = _cache(apc, n, n_slots, frac, rng)
+    s, idx = _lists(rng, b, ld, n)
+    os_ = torch.full((b,), 7.0, device="cuda")
+    oi = torch.full((b,), 7, dtype=torch.int32, device="cuda")
+    apc.apc_resident_best(c, torch.from_numpy(s).cuda(), torch.from_numpy(idx).cuda(), ld, k, b, os_, oi)
+    torch.cuda.synchronize()
+    ws, wi = orc.resident_best(s, idx, k, soe, n_slots)
+    gs, gi = os_.cpu().numpy(), oi.cpu().numpy()
+    assert np.array_equal(gi, wi)
+    assert np.array_equal(np.isnan(gs), np.isnan(ws)) and np.array_equal(gs[~np.isnan(ws)], ws[~np.isnan(ws)])
+    c.close()
+
+
+def test_resident_best_without_slot_map(apc, orc):
+    say("resident_best without slot map")
+    rng = np.random.default_rng(77)
+    n = 500
+    c, _ = _cache(apc, n, n, 1.0, rng, with_map=False)
+    s, idx = _lists(rng, 300, 8, n)
+    os_ = torch.empty(300, device="cuda")
+    oi = torch.empty(300, dtype=torch.int32, device="cuda")
+    apc.apc_resident_best(c, torch.from_numpy(s).cuda(), torch.from_numpy(idx).cuda(), 8, 8, 300, os_, oi)
+    torch.cuda.synchronize()
+    ws, wi = orc.resident_best(s, idx, 8, None, n)
+    assert np.array_equal(oi.cpu().numpy(), wi)
+    c.close()
+
+
+def test_resident_fallback_end_to_end(apc, orc):
+    say("resident fallback after match")
+    rng = np.random.default_rng(78)
+    n, d, b, k, n_slots = 6000, 128, 300, 16, 300
+    e, _ = make_rows(n, d, "f16", 11, clusters=40)
+    q, _ = make_rows(b, d, "f16", 12, clusters=40)
+    soe = np.full(n, -1, np.int32)
+    soe[rng.choice(n, n_slots, replace=False)] = np.arange(n_slots)
+    pool = torch.zeros((n_slots, 16), dtype=torch.uint8, device="cuda")
+    c = apc.apc_build_cache(e, None, pool, torch.from_numpy(soe).cuda())
+    ts = torch.empty((b, k), device="cuda")
+    ti = torch.empty((b, k), dtype=torch.int32, device="cuda")
+    ws = apc.workspace_tensor(c, b, k)
+    apc.apc_match_batch(c, q, None, k, ts, ti, ws)
+    os_ = torch.empty(b, device="cuda")
+    oi = torch.empty(b, dtype=torch.int32, device="cuda")
+    apc.apc_resident_best(c, ts, ti, k, k, b, os_, oi)
+    torch.cuda.synchronize()
+    rs, ri = orc.topk("f16", stored_np(q), None, stored_np(e), None, k)
+    want_s, want_i = orc.resident_best(rs.astype(np.float32), ri, k, soe, n_slots)
+    same = np.all(ti.cpu().numpy() == ri, axis=1)            # rows whose neighbour lists agree
+    assert same.mean() > 0.9
+    gi, gs = oi.cpu().numpy(), os_.cpu().numpy()
+    assert np.array_equal(gi[same], want_i[same])
+    found = same & (want_i >= 0)
+    assert found.sum() > 0 and (want_i[same] < 0).sum() > 0
+    assert np.all(np.abs(gs[found] - want_s[found]) <= TOL["f16"])
+    c.close()
+
+
+@pytest.mark.parametrize("b,L", [(0, 3), (1, 0), (1000, 5), (5000, 32), (16384, 10)])
+def test_level_histogram_bit_exact(apc, orc, b, L):
+    say(f"level_histogram b={b} L={L}")
+    rng = np.random.default_rng(b + L)
+    lv = rng.integers(-1, L + 2, b).astype(np.int32)
+    if b > 10:
+        lv[: b // 2] = L // 2                                  # one heavy level
+    hist = torch.full((L + 1,), -7, dtype=torch.int32, device="cuda")
+    apc.apc_level_histogram(torch.from_numpy(lv).cuda() if b else torch.empty(1, dtype=torch.int32, device="cuda"),
+                            b, L, hist)
+    torch.cuda.synchronize()
+    assert np.array_equal(hist.cpu().numpy(), orc.level_histogram(lv, L))
