@@ -219,6 +219,13 @@ def main():
     ap.add_argument("--resident-fallback", action="store_true",
                     help="level and latent follow the best neighbour whose latent is resident "
                          "(apc_resident_best) instead of the top-1")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="consecutive batches of the timed steps alternate over this many streams, each with "
+                         "its own buffers, so one batch's latency-bound tail overlaps the next batch's work")
+    ap.add_argument("--overlap-streams", type=int, default=0,
+                    help="also time the steps with consecutive batches over this many streams and report it "
+                         "under 'overlapped' (off by default: its stretched similarity-kernel launches would "
+                         "enter a kernel trace of the default command)")
     ap.add_argument("--sweep", action="store_true",
                     help="only run the small-batch streaming sweep: the b1024 (bf16) and b16384 (e4m3) "
                          "caches against B = 1 ... 256 queries, one JSON line per point")
@@ -257,13 +264,22 @@ def main():
     copies = args.copies or (1 if cache_bytes > MALL_BYTES else min(8, -(-(5 * MALL_BYTES) // cache_bytes)))
     embs = [e] + [e.clone() for _ in range(copies - 1)]
     caches = [apc.apc_build_cache(x, es, pool, soe) for x in embs]
-    step = apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes,
-                         route=args.route, resident_fallback=args.resident_fallback)
+    steps = [apc.MatchStep(caches[0], w.B, w.k, theta, K, lvl, cap, queue, latent_bytes=w.latent_bytes,
+                           route=args.route, resident_fallback=args.resident_fallback)
+             for _ in range(max(1, args.streams, args.overlap_streams))]
+    step = steps[0]
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(len(steps) - 1)]
     torch.cuda.synchronize()
 
     def run(i):
         step.cache = caches[i % copies]
         step.run(q, qs)
+
+    def run_overlapped(i, n_streams):
+        # batch i on stream i mod S with its own buffers; batches are independent
+        st = steps[i % n_streams]
+        st.cache = caches[i % copies]
+        st.run(q, qs, stream=streams[i % n_streams])
 
     log(f"warmup {args.warmup} steps, {copies} cache copies")
     for i in range(args.warmup):
@@ -292,12 +308,18 @@ def main():
         for i in range(max(args.warmup, copies)):
             graphs[i % copies].replay()
         torch.cuda.synchronize()
+    if args.streams > 1:
+        for i in range(args.warmup):
+            run_overlapped(i, args.streams)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        if graphs is None:
-            run(i)
-        else:
+        if graphs is not None:
             graphs[i % copies].replay()
+        elif args.streams > 1:
+            run_overlapped(i, args.streams)
+        else:
+            run(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     wall = t1 - t0
@@ -317,6 +339,19 @@ def main():
     ev.close()
     spread = {"p10": round(step_ms[ns // 10], 4), "p50": round(float(np.median(step_ms)), 4),
               "p90": round(step_ms[(9 * ns) // 10], 4), "steps": ns}
+    # the same steps with consecutive batches overlapped over several streams
+    overlapped = None
+    if args.overlap_streams > 1 and graphs is None:
+        for i in range(args.warmup):
+            run_overlapped(i, args.overlap_streams)
+        torch.cuda.synchronize()
+        to = time.perf_counter()
+        for i in range(args.steps):
+            run_overlapped(i, args.overlap_streams)
+        torch.cuda.synchronize()
+        wo = time.perf_counter() - to
+        overlapped = {"streams": args.overlap_streams, "value": round(w.B * args.steps / wo, 1),
+                      "ms_per_step": round(wo / args.steps * 1e3, 4)}
     # share of the batch that starts from a gathered latent (last step)
     hit_rate = round(float(step.hit.float().mean().item()), 4) if step.batch is not None else None
     # the placement kernel alone (on the last step's scores)
@@ -371,13 +406,14 @@ def main():
         "config": {"workload": w.name, "B": w.B, "N": w.N, "d": w.d, "k": w.k, "levels": w.L,
                    "instances": w.n_inst, "capacity": w.cap, "latent_bytes": w.latent_bytes,
                    "cache_copies": copies, "launch": "hip_graph" if args.graph else "eager",
-                   "route": args.route, "resident_fallback": args.resident_fallback},
+                   "route": args.route, "resident_fallback": args.resident_fallback, "streams": args.streams},
         "sims_per_s": round(w.B * w.N / (kern_ms * 1e-3), 1),
         "sim_kernel_ms": round(kern_ms, 5),
         "step_ms_spread": spread,
         "warm_ms_per_step": warm,
         "assign_ms": round(assign_ms, 5),
         "latent_hit_rate": hit_rate,
+        "overlapped": overlapped,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

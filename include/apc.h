@@ -15,6 +15,9 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Calls enqueue work on it and return without waiting, except
  *    apc_build_cache, which waits once to report data errors.
+ *  - Calls keep no device state of their own between or across calls: calls
+ *    on different streams may run concurrently when their output and
+ *    workspace buffers are distinct (one cache handle may serve them all).
  *  - Arguments are checked on the host before anything is enqueued; on a
  *    non-OK status nothing was enqueued and no output was written, except
  *    APC_E_HIP (a launch failed; outputs are unspecified).
