@@ -332,3 +332,32 @@ def level_histogram(level, L: int):
         if 0 <= v <= L:
             H[v] += 1
     return H
+
+
+# ---- Latents per (entry, level) ---------------------------------------------
+# The state after K skipped steps depends on K.  Reading: a resident entry
+# holds one latent per level 1..levels_per_slot, stored level-major inside its
+# slot (pool row slot * levels_per_slot + level - 1); a query placed at level
+# l > 0 copies its entry's latent of level l.  levels_per_slot = 1 keeps one
+# latent per entry, used for every level.
+
+def gather_at_level(top1, out_level, out_inst, out_slot, slot_of_entry, n_entries, pool: np.ndarray,
+                    levels_per_slot: int, n_inst: int, slots_per_inst: int, batch: np.ndarray):
+    """Copies into `batch` in place; returns hit (int32)."""
+    pool = np.asarray(pool, dtype=np.uint8)
+    n_ent_slots = pool.shape[0] // levels_per_slot
+    b = len(top1)
+    hit = np.zeros(b, dtype=np.int32)
+    for q in range(b):
+        lvl, e = int(out_level[q]), int(top1[q])
+        if lvl <= 0 or e < 0 or e >= n_entries:
+            continue
+        if levels_per_slot > 1 and lvl > levels_per_slot:
+            continue
+        slot = e if slot_of_entry is None else int(slot_of_entry[e])
+        if slot < 0 or slot >= n_ent_slots:
+            continue
+        row = slot * levels_per_slot + (0 if levels_per_slot == 1 else lvl - 1)
+        batch[int(out_inst[q]) * slots_per_inst + int(out_slot[q])] = pool[row]
+        hit[q] = 1
+    return hit

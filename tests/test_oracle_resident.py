@@ -60,3 +60,48 @@ def test_level_histogram_is_bincount():
         ok = lv[(lv >= 0) & (lv <= L)]
         assert np.array_equal(H, np.bincount(ok, minlength=L + 1)[: L + 1])
         assert H.sum() == ok.size
+
+
+def test_gather_at_level_one_latent_per_entry_is_gather():
+    rng = np.random.default_rng(44)
+    n, n_slots, lb, b, n_inst, spi = 400, 90, 32, 120, 4, 40
+    pool = rng.integers(0, 256, (n_slots, lb), dtype=np.uint8)
+    soe = np.full(n, -1, np.int32)
+    soe[rng.choice(n, n_slots, replace=False)] = np.arange(n_slots)
+    top1 = rng.integers(-1, n, b)
+    perm = rng.permutation(n_inst * spi)[:b]
+    ol = rng.integers(-1, 4, b).astype(np.int32)
+    oi, os_ = (perm // spi).astype(np.int32), (perm % spi).astype(np.int32)
+    want = np.zeros((n_inst * spi, lb), np.uint8)
+    got = np.zeros_like(want)
+    h1 = oracle.gather(top1, ol, oi, os_, soe, n, pool, n_inst, spi, want)
+    h2 = oracle.gather_at_level(top1, ol, oi, os_, soe, n, pool, 1, n_inst, spi, got)
+    assert np.array_equal(h1, h2) and np.array_equal(want, got) and h1.sum() > 0
+
+
+def test_gather_at_level_reads_the_level_row():
+    # every pool row holds its own (slot, level) code, so the copy names its source
+    rng = np.random.default_rng(45)
+    n, S, Lp, b, n_inst, spi = 300, 50, 5, 200, 3, 80
+    pool = np.zeros((S * Lp, 16), np.uint8)
+    for s in range(S):
+        for lv in range(1, Lp + 1):
+            pool[s * Lp + lv - 1, :2] = (s, lv)
+    soe = np.full(n, -1, np.int32)
+    ent = rng.choice(n, S, replace=False)
+    soe[ent] = np.arange(S)
+    top1 = rng.integers(0, n, b)
+    top1[: b // 2] = ent[rng.integers(0, S, b // 2)]
+    ol = rng.integers(-1, Lp + 2, b).astype(np.int32)
+    perm = rng.permutation(n_inst * spi)[:b]
+    oi, os_ = (perm // spi).astype(np.int32), (perm % spi).astype(np.int32)
+    batch = np.full((n_inst * spi, 16), 255, np.uint8)
+    hit = oracle.gather_at_level(top1, ol, oi, os_, soe, n, pool, Lp, n_inst, spi, batch)
+    for q in range(b):
+        ok = 1 <= ol[q] <= Lp and soe[top1[q]] >= 0
+        assert hit[q] == ok
+        row = batch[oi[q] * spi + os_[q]]
+        if ok:
+            assert tuple(row[:2]) == (soe[top1[q]], ol[q])
+        else:
+            assert (row == 255).all()
