@@ -265,6 +265,23 @@ apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_
                               void* batch_latents, int32_t* hit, void* stream);
 
 /*
+ * Latent gather at the assigned level (the cached state after K skipped steps
+ * depends on K, Introduction and Approach): as apc_gather_latents, with
+ * levels_per_slot latents per resident slot of cache c, level-major inside the
+ * slot: the latent of slot s at level l is latents row s * levels_per_slot +
+ * l - 1.  A query placed at level l > 0 copies its entry's latent of level l
+ * (no copy, hit = 0, when l > levels_per_slot).  levels_per_slot = 1 is
+ * apc_gather_latents (one latent per entry, used at every level).  The
+ * cache's n_slots counts latents, so it must be a multiple of levels_per_slot,
+ * and slot_of_entry values index the n_slots / levels_per_slot entry slots
+ * (larger ones are not resident).  1 <= levels_per_slot <= APC_MAX_LEVELS.
+ */
+apc_status apc_gather_latents_at_level(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
+                                       const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                                       int32_t n_inst, int32_t slots_per_inst, int32_t levels_per_slot,
+                                       void* batch_latents, int32_t* hit, void* stream);
+
+/*
  * Measurement hook (for benchmarks and profilers, not for the method):
  * the next apc_match_batch call on this thread records `start` (a
  * hipEvent_t) on its stream right before the similarity/top-k kernel and

@@ -72,6 +72,8 @@ def load() -> ctypes.CDLL:
     L.apc_resident_best.restype = st
     L.apc_level_histogram.argtypes = [vp, i32, i32, vp, vp]
     L.apc_level_histogram.restype = st
+    L.apc_gather_latents_at_level.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, vp]
+    L.apc_gather_latents_at_level.restype = st
     L.apc_gather_latents.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, vp, vp, vp]
     L.apc_gather_latents.restype = st
     L.apc_set_kernel_events.argtypes = [vp, vp]
@@ -272,3 +274,11 @@ def apc_gather_latents(c: Cache, top_idx: torch.Tensor, ld: int, b: int, out_lev
     _check(load().apc_gather_latents(c.handle, _ptr(top_idx), ld, b, _ptr(out_level), _ptr(out_inst),
                                      _ptr(out_slot), n_inst, slots_per_inst, _ptr(batch_latents),
                                      _ptr(hit), _stream(stream)))
+
+
+def apc_gather_latents_at_level(c: Cache, top_idx: torch.Tensor, ld: int, b: int, out_level: torch.Tensor,
+                                out_inst: torch.Tensor, out_slot: torch.Tensor, n_inst: int, slots_per_inst: int,
+                                levels_per_slot: int, batch_latents: torch.Tensor, hit: torch.Tensor, stream=None):
+    _check(load().apc_gather_latents_at_level(c.handle, _ptr(top_idx), ld, b, _ptr(out_level), _ptr(out_inst),
+                                              _ptr(out_slot), n_inst, slots_per_inst, levels_per_slot,
+                                              _ptr(batch_latents), _ptr(hit), _stream(stream)))

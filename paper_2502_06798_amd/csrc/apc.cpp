@@ -428,25 +428,46 @@ apc_status apc_level_histogram(const int32_t* level, int32_t b, int32_t L, int32
     return ok();
 }
 
+static apc_status gather_impl(const char* who, const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
+                              const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                              int32_t n_inst, int32_t slots_per_inst, int32_t lps, void* batch_latents,
+                              int32_t* hit, void* stream)
+{
+    if (!c) return fail(APC_E_ARG, "%s: NULL cache", who);
+    if (c->n_slots == 0) return fail(APC_E_ARG, "%s: the cache has no latents", who);
+    if (b < 0 || ld < 1 || n_inst < 0 || slots_per_inst < 0)
+        return fail(APC_E_ARG, "%s: need b >= 0, ld >= 1, n_inst >= 0, slots_per_inst >= 0", who);
+    if (lps < 1 || lps > APC_MAX_LEVELS || c->n_slots % lps != 0)
+        return fail(APC_E_ARG, "%s: levels_per_slot must be in 1..%d and divide the cache's %lld latents", who,
+                    APC_MAX_LEVELS, (long long)c->n_slots);
+    if (b == 0) return ok();
+    if (!top_idx || !out_level || !out_inst || !out_slot || !hit)
+        return fail(APC_E_ARG, "%s: NULL device buffer", who);
+    if ((int64_t)n_inst * slots_per_inst > 0 && (!batch_latents || !aligned16(batch_latents)))
+        return fail(APC_E_ARG, "%s: batch_latents must be 16-byte aligned", who);
+    hipError_t e = apc::launch_gather(c->latents, c->n, c->n_slots, c->latent_bytes, c->slot_of_entry,
+                                      top_idx, ld, b, out_level, out_inst, out_slot, n_inst, slots_per_inst, lps,
+                                      batch_latents, hit, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
 apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
                               const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
                               int32_t n_inst, int32_t slots_per_inst, void* batch_latents, int32_t* hit,
                               void* stream)
 {
-    if (!c) return fail(APC_E_ARG, "apc_gather_latents: NULL cache");
-    if (c->n_slots == 0) return fail(APC_E_ARG, "apc_gather_latents: the cache has no latents");
-    if (b < 0 || ld < 1 || n_inst < 0 || slots_per_inst < 0)
-        return fail(APC_E_ARG, "apc_gather_latents: need b >= 0, ld >= 1, n_inst >= 0, slots_per_inst >= 0");
-    if (b == 0) return ok();
-    if (!top_idx || !out_level || !out_inst || !out_slot || !hit)
-        return fail(APC_E_ARG, "apc_gather_latents: NULL device buffer");
-    if ((int64_t)n_inst * slots_per_inst > 0 && (!batch_latents || !aligned16(batch_latents)))
-        return fail(APC_E_ARG, "apc_gather_latents: batch_latents must be 16-byte aligned");
-    hipError_t e = apc::launch_gather(c->latents, c->n, c->n_slots, c->latent_bytes, c->slot_of_entry,
-                                      top_idx, ld, b, out_level, out_inst, out_slot, n_inst, slots_per_inst,
-                                      batch_latents, hit, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "apc_gather_latents launch");
-    return ok();
+    return gather_impl("apc_gather_latents", c, top_idx, ld, b, out_level, out_inst, out_slot, n_inst,
+                       slots_per_inst, 1, batch_latents, hit, stream);
+}
+
+apc_status apc_gather_latents_at_level(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
+                                       const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
+                                       int32_t n_inst, int32_t slots_per_inst, int32_t levels_per_slot,
+                                       void* batch_latents, int32_t* hit, void* stream)
+{
+    return gather_impl("apc_gather_latents_at_level", c, top_idx, ld, b, out_level, out_inst, out_slot, n_inst,
+                       slots_per_inst, levels_per_slot, batch_latents, hit, stream);
 }
 
 }  // extern "C"

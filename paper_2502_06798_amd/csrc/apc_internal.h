@@ -119,7 +119,7 @@ hipError_t launch_level_histogram(const int32_t* level, int32_t b, int32_t L, in
 hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,
                          const int32_t* slot_of_entry, const int32_t* top_idx, int32_t ld, int32_t b,
                          const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
-                         int32_t n_inst, int32_t slots_per_inst, void* batch, int32_t* hit,
+                         int32_t n_inst, int32_t slots_per_inst, int32_t lps, void* batch, int32_t* hit,
                          hipStream_t s);
 
 }  // namespace apc

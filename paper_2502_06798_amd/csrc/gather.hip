@@ -1,5 +1,7 @@
 // Latent gather: copy the cached latent of each placed query's nearest entry
-// into its (instance, slot) of the batch buffer.  One workgroup per query,
+// into its (instance, slot) of the batch buffer.  A slot holds lps latents:
+// one for every level (lps = 1), or one per level 1..lps, level-major inside
+// the slot (pool row slot * lps + level - 1).  One workgroup per query,
 // 16-byte loads and stores spread over the workgroup so every wavefront
 // moves 1 KiB contiguous per instruction.
 #include "apc_internal.h"
@@ -14,17 +16,18 @@ __global__ __launch_bounds__(256) void k_gather(const uint8_t* __restrict__ pool
                                                 const int32_t* __restrict__ out_level,
                                                 const int32_t* __restrict__ out_inst,
                                                 const int32_t* __restrict__ out_slot, int32_t n_inst,
-                                                int32_t slots_per_inst, uint8_t* __restrict__ batch,
-                                                int32_t* __restrict__ hit)
+                                                int32_t slots_per_inst, int32_t lps,
+                                                uint8_t* __restrict__ batch, int32_t* __restrict__ hit)
 {
     const int64_t q = blockIdx.x;
     const int32_t e = top_idx[q * ld];
     const int32_t lvl = out_level[q], inst = out_inst[q], slot = out_slot[q];
     int64_t src = -1;
-    if (lvl > 0 && e >= 0 && e < n_entries && inst >= 0 && inst < n_inst && slot >= 0 &&
-        slot < slots_per_inst) {
+    if (lvl > 0 && (lps == 1 || lvl <= lps) && e >= 0 && e < n_entries && inst >= 0 && inst < n_inst &&
+        slot >= 0 && slot < slots_per_inst) {
         src = slot_of_entry ? (int64_t)slot_of_entry[e] : (int64_t)e;
-        if (src >= n_slots) src = -1;
+        if (src >= n_slots / lps) src = -1;
+        else if (src >= 0 && lps > 1) src = src * lps + (lvl - 1);
     }
     if (threadIdx.x == 0) hit[q] = src >= 0 ? 1 : 0;
     if (src < 0) return;
@@ -39,13 +42,13 @@ __global__ __launch_bounds__(256) void k_gather(const uint8_t* __restrict__ pool
 hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,
                          const int32_t* slot_of_entry, const int32_t* top_idx, int32_t ld, int32_t b,
                          const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
-                         int32_t n_inst, int32_t slots_per_inst, void* batch, int32_t* hit,
+                         int32_t n_inst, int32_t slots_per_inst, int32_t lps, void* batch, int32_t* hit,
                          hipStream_t s)
 {
     if (b <= 0) return hipSuccess;
     k_gather<<<(unsigned)b, 256, 0, s>>>(static_cast<const uint8_t*>(pool), n_entries, n_slots,
                                          latent_bytes, slot_of_entry, top_idx, ld, out_level, out_inst,
-                                         out_slot, n_inst, slots_per_inst, static_cast<uint8_t*>(batch), hit);
+                                         out_slot, n_inst, slots_per_inst, lps, static_cast<uint8_t*>(batch), hit);
     return hipGetLastError();
 }
 

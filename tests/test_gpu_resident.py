@@ -123,3 +123,38 @@ def test_level_histogram_bit_exact(apc, orc, b, L):
                             b, L, hist)
     torch.cuda.synchronize()
     assert np.array_equal(hist.cpu().numpy(), orc.level_histogram(lv, L))
+
+
+@pytest.mark.parametrize("lps,b", [(1, 300), (5, 300), (10, 2000), (32, 64)])
+def test_gather_at_level_bit_exact(apc, orc, lps, b):
+    say(f"gather_at_level lps={lps} b={b}")
+    rng = np.random.default_rng(90 + lps)
+    n, S, lb, n_inst, spi = 3000, 200, 4096 + 32, 6, 512
+    e, _ = make_rows(n, 64, "f16", 13)
+    pool_h = rng.integers(0, 256, (S * lps, lb), dtype=np.uint8)
+    pool = torch.from_numpy(pool_h).cuda()
+    soe = np.full(n, -1, np.int32)
+    ent = rng.choice(n, S, replace=False)
+    soe[ent] = np.arange(S)
+    c = apc.apc_build_cache(e, None, pool, torch.from_numpy(soe).cuda())
+    top = rng.integers(0, n, (b, 3)).astype(np.int32)
+    top[: b // 2, 0] = ent[rng.integers(0, S, b // 2)]
+    perm = rng.permutation(n_inst * spi)[:b]
+    ol = rng.integers(-1, max(lps, 4) + 2, b).astype(np.int32)
+    oi, os_ = (perm // spi).astype(np.int32), (perm % spi).astype(np.int32)
+    oi[ol < 0] = -1
+    os_[ol < 0] = -1
+    batch = torch.zeros((n_inst * spi, lb), dtype=torch.uint8, device="cuda")
+    hit = torch.empty(b, dtype=torch.int32, device="cuda")
+    cu = lambda a: torch.from_numpy(a).cuda()
+    apc.apc_gather_latents_at_level(c, cu(top), 3, b, cu(ol), cu(oi), cu(os_), n_inst, spi, lps, batch, hit)
+    torch.cuda.synchronize()
+    want = np.zeros((n_inst * spi, lb), np.uint8)
+    h = orc.gather_at_level(top[:, 0], ol, oi, os_, soe, n, pool_h, lps, n_inst, spi, want)
+    assert np.array_equal(hit.cpu().numpy(), h) and h.sum() > 0
+    assert np.array_equal(batch.cpu().numpy(), want)
+    if lps > 1:                                               # n_slots must be a multiple of levels_per_slot
+        with pytest.raises(apc.ApcError):
+            apc.apc_gather_latents_at_level(c, cu(top), 3, b, cu(ol), cu(oi), cu(os_), n_inst, spi, 7, batch,
+                                            hit)
+    c.close()
