@@ -144,3 +144,45 @@ def test_assign_planned_is_optimal(apc, orc, b, L, I, tight):
     again = _run(apc, apc.apc_assign_routed, best, 1, theta, K, il, ic, iq, plan)
     for a, e in zip(again, (opt, ol, oi, os_, fill)):
         assert np.array_equal(a, e)
+
+
+def test_plan_placement_edge_cases(apc, orc):
+    say("plan placement edge cases")
+    theta, K = [0.0, 0.5], [4, 9]
+    b = 40
+    ts = torch.linspace(-1, 1, b).reshape(b, 1).cuda()
+    outs = lambda: [torch.full((b,), -7, dtype=torch.int32, device="cuda") for _ in range(4)]
+    plan = torch.full((9,), -7, dtype=torch.int32, device="cuda")
+    # no capacity anywhere: nothing served, the plan is all zeros
+    o = outs()
+    fill = torch.full((2,), -7, dtype=torch.int32, device="cuda")
+    apc.apc_assign_planned(ts, 1, b, theta, K, [0, 2], [0, 0], None, plan, *o, fill)
+    torch.cuda.synchronize()
+    assert (plan == 0).all() and (o[1] == -1).all() and (fill == 0).all()
+    # no instances at all
+    o = outs()
+    apc.apc_assign_planned(ts, 1, b, theta, K, [], [], None, plan, *o, fill)
+    torch.cuda.synchronize()
+    assert (plan == 0).all() and (o[1] == -1).all() and (o[2] == -1).all()
+    # empty batch: the plan is written (zeros), the instance fills are zero
+    apc.apc_assign_planned(ts, 1, 0, theta, K, [0, 1], [3, 3], None, plan, *outs(), fill)
+    torch.cuda.synchronize()
+    assert (plan == 0).all() and (fill == 0).all()
+    # capacity exactly the demand, one level only: everything goes there
+    o = outs()
+    fill1 = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    apc.apc_assign_planned(ts, 1, b, theta, K, [2], [b], None, plan, *o, fill1)
+    torch.cuda.synchronize()
+    lv = orc.levels(ts[:, 0].cpu().numpy().astype(np.float64), np.array(theta, np.float32))
+    Xo = np.zeros((3, 3), dtype=np.int64)                     # the only optimal plan here
+    Xo[:, 2] = orc.level_histogram(lv, 2)
+    assert np.array_equal(plan.cpu().numpy().reshape(3, 3), Xo) and (o[1] == 2).all() and fill1.item() == b
+    r = orc.assign_routed(lv, 2, Xo, [2], [b], None)
+    assert np.array_equal(o[2].cpu().numpy(), r[1]) and np.array_equal(o[3].cpu().numpy(), r[2])
+    # a caller's plan of all zeros routes nothing
+    o = outs()
+    apc.apc_assign_routed(ts, 1, b, theta, K, [0, 1, 2], [9, 9, 9], None,
+                          torch.zeros(9, dtype=torch.int32, device="cuda"), *o,
+                          torch.empty(3, dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    assert (o[1] == -1).all()
