@@ -361,3 +361,29 @@ def gather_at_level(top1, out_level, out_inst, out_slot, slot_of_entry, n_entrie
         batch[int(out_inst[q]) * slots_per_inst + int(out_slot[q])] = pool[row]
         hit[q] = 1
     return hit
+
+
+# ---- Merging the top-k lists of cache shards --------------------------------
+# With the cache split by rows over several devices, each shard's top-k uses
+# its local entry numbers; an entry's global number is its shard's offset plus
+# the local one.  The global top-k is the top-k of the union of the shards'
+# lists under the total order (score desc, global entry asc), since every
+# member of the global top-k is in its own shard's top-k.
+
+def merge_shards(scores, idx, offsets, k: int):
+    """scores/idx: (g, b, k_in) lists, best first; offsets: g global offsets.
+    Returns (score float32 [b, k], entry int32 [b, k]); slots past the valid
+    candidates (entries < 0 or NaN scores are not candidates) hold NaN / -1."""
+    scores = np.asarray(scores, dtype=np.float32)
+    idx = np.asarray(idx, dtype=np.int64)
+    g, b, kin = idx.shape
+    out_s = np.full((b, k), np.nan, dtype=np.float32)
+    out_i = np.full((b, k), -1, dtype=np.int32)
+    for q in range(b):
+        cand = [(float(scores[s, q, j]), int(idx[s, q, j]) + int(offsets[s]))
+                for s in range(g) for j in range(kin)
+                if idx[s, q, j] >= 0 and not np.isnan(scores[s, q, j])]
+        cand.sort(key=lambda c: (-c[0], c[1]))
+        for j, (sc, e) in enumerate(cand[:k]):
+            out_s[q, j], out_i[q, j] = sc, e
+    return out_s, out_i
