@@ -198,6 +198,38 @@ def sweep():
         torch.cuda.empty_cache()
 
 
+def shard_merge(w, g, steps):
+    """Times the merge of g shards' sorted top-k lists (seeded scores) for the
+    workload's batch; bytes = the lists read once plus the result written."""
+    import numpy as np
+    import torch
+
+    import paper_2502_06798_amd as apc
+    apc.load()
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    sc = torch.rand((g, w.B, w.k), device="cuda", generator=gen).sort(dim=2, descending=True).values
+    ix = torch.randint(0, w.N // g, (g, w.B, w.k), device="cuda", generator=gen, dtype=torch.int32)
+    offs = [a * (w.N // g) for a in range(g)]
+    os_ = torch.empty((w.B, w.k), device="cuda")
+    oi = torch.empty((w.B, w.k), dtype=torch.int32, device="cuda")
+    for _ in range(5):
+        apc.apc_merge_shards(sc, ix, g, w.B, w.k, offs, w.k, os_, oi)
+    ev = HipEvents(steps)
+    ev.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    cur = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for i in range(steps):
+        ev.hip.hipEventRecord(ev.pairs[i][0], cur)
+        apc.apc_merge_shards(sc, ix, g, w.B, w.k, offs, w.k, os_, oi)
+        ev.hip.hipEventRecord(ev.pairs[i][1], cur)
+    torch.cuda.synchronize()
+    ms = float(np.median([ev.elapsed_ms(i) for i in range(steps)]))
+    ev.close()
+    nbytes = 8 * w.B * w.k * (g + 1)
+    print(json.dumps({"kernel": "k_merge_shards", "workload": w.name, "shards": g, "B": w.B, "k": w.k,
+                      "ms": round(ms, 5), "bytes": nbytes, "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,6 +258,9 @@ def main():
                     help="also time the steps with consecutive batches over this many streams and report it "
                          "under 'overlapped' (off by default: its stretched similarity-kernel launches would "
                          "enter a kernel trace of the default command)")
+    ap.add_argument("--shard-merge", type=int, default=0, metavar="G",
+                    help="only time apc_merge_shards: G shards' top-k lists of the workload's batch "
+                         "(the merge each device runs after exchanging them), one JSON line")
     ap.add_argument("--sweep", action="store_true",
                     help="only run the small-batch streaming sweep: the b1024 (bf16) and b16384 (e4m3) "
                          "caches against B = 1 ... 256 queries, one JSON line per point")
@@ -247,6 +282,9 @@ def main():
         return
     if args.sweep:
         sweep()
+        return
+    if args.shard_merge:
+        shard_merge(synth.BY_NAME[args.workload], args.shard_merge, args.steps)
         return
     apc.load()
     w = synth.BY_NAME[args.workload]

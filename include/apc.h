@@ -58,6 +58,7 @@ typedef enum {
 #define APC_MAX_K 64          /* largest neighbour count per query */
 #define APC_MAX_LEVELS 32     /* largest number of skip levels L */
 #define APC_MAX_INST 256      /* largest number of model instances */
+#define APC_MAX_SHARDS 64     /* largest number of row shards apc_merge_shards merges */
 #define APC_MAX_ROUTED_BATCH 16384  /* largest batch of apc_assign_routed / apc_assign_planned */
 
 /* opaque, immutable after build */
@@ -280,6 +281,25 @@ apc_status apc_gather_latents_at_level(const apc_cache* c, const int32_t* top_id
                                        const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
                                        int32_t n_inst, int32_t slots_per_inst, int32_t levels_per_slot,
                                        void* batch_latents, int32_t* hit, void* stream);
+
+/*
+ * Merge of the top-k lists of row shards of one cache (the cache split by
+ * rows over g devices: each runs apc_match_batch on its shard, the lists are
+ * exchanged, and every device merges them).  scores / idx: g x b x k_in
+ * lists as the shards' apc_match_batch calls wrote them (shard s's block at
+ * s * b * k_in, best first, entries local to the shard), contiguous as an
+ * all-gather leaves them.  offsets (host) g global entry numbers of the
+ * shards' first rows.  out_score / out_idx: b x k, the best k of all shards'
+ * candidates under (score desc, global entry asc); entries < 0 and NaN
+ * scores are not candidates, and slots past the last candidate get NaN / -1.
+ * Since every entry of the whole cache's top-k is in its shard's top-k, the
+ * merge of the shards' top-k lists is the whole cache's top-k.
+ * 1 <= g <= APC_MAX_SHARDS, 1 <= k, k_in <= APC_MAX_K, offsets >= 0, and the
+ * global entry numbers must fit in int32.  Errors: APC_E_ARG.
+ */
+apc_status apc_merge_shards(const float* scores, const int32_t* idx, int32_t g, int32_t b, int32_t k_in,
+                            const int32_t* offsets /* host */, int32_t k, float* out_score, int32_t* out_idx,
+                            void* stream);
 
 /*
  * Measurement hook (for benchmarks and profilers, not for the method):

@@ -74,6 +74,8 @@ def load() -> ctypes.CDLL:
     L.apc_level_histogram.restype = st
     L.apc_gather_latents_at_level.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, vp]
     L.apc_gather_latents_at_level.restype = st
+    L.apc_merge_shards.argtypes = [vp, vp, i32, i32, i32, vp, i32, vp, vp, vp]
+    L.apc_merge_shards.restype = st
     L.apc_gather_latents.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, i32, vp, vp, vp]
     L.apc_gather_latents.restype = st
     L.apc_set_kernel_events.argtypes = [vp, vp]
@@ -282,3 +284,12 @@ def apc_gather_latents_at_level(c: Cache, top_idx: torch.Tensor, ld: int, b: int
     _check(load().apc_gather_latents_at_level(c.handle, _ptr(top_idx), ld, b, _ptr(out_level), _ptr(out_inst),
                                               _ptr(out_slot), n_inst, slots_per_inst, levels_per_slot,
                                               _ptr(batch_latents), _ptr(hit), _stream(stream)))
+
+
+def apc_merge_shards(scores: torch.Tensor, idx: torch.Tensor, g: int, b: int, k_in: int, offsets: Sequence[int],
+                     k: int, out_score: torch.Tensor, out_idx: torch.Tensor, stream=None):
+    off = _host(offsets, np.int32)
+    if off is None or off.size != g:
+        raise ValueError("apc_merge_shards: need one offset per shard")
+    _check(load().apc_merge_shards(_ptr(scores), _ptr(idx), g, b, k_in, _hp(off), k, _ptr(out_score),
+                                   _ptr(out_idx), _stream(stream)))

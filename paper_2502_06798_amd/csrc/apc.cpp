@@ -428,6 +428,26 @@ apc_status apc_level_histogram(const int32_t* level, int32_t b, int32_t L, int32
     return ok();
 }
 
+apc_status apc_merge_shards(const float* scores, const int32_t* idx, int32_t g, int32_t b, int32_t k_in,
+                            const int32_t* offsets, int32_t k, float* out_score, int32_t* out_idx, void* stream)
+{
+    if (g < 1 || g > APC_MAX_SHARDS || b < 0 || k < 1 || k > APC_MAX_K || k_in < 1 || k_in > APC_MAX_K)
+        return fail(APC_E_ARG, "apc_merge_shards: need 1 <= g <= %d, b >= 0, 1 <= k, k_in <= %d", APC_MAX_SHARDS,
+                    APC_MAX_K);
+    if (!offsets) return fail(APC_E_ARG, "apc_merge_shards: offsets is NULL");
+    apc::ShardOffsets off{};
+    for (int s = 0; s < g; ++s) {
+        if (offsets[s] < 0) return fail(APC_E_ARG, "apc_merge_shards: offsets[%d] < 0", s);
+        off.v[s] = offsets[s];
+    }
+    if (b == 0) return ok();
+    if (!scores || !idx || !out_score || !out_idx) return fail(APC_E_ARG, "apc_merge_shards: NULL device buffer");
+    hipError_t e = apc::launch_merge_shards(scores, idx, g, b, k_in, off, k, out_score, out_idx,
+                                            static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_merge_shards launch");
+    return ok();
+}
+
 static apc_status gather_impl(const char* who, const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
                               const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
                               int32_t n_inst, int32_t slots_per_inst, int32_t lps, void* batch_latents,

@@ -115,6 +115,13 @@ hipError_t launch_resident_best(const int32_t* slot_of_entry, int64_t n_entries,
                                 float* out_score, int32_t* out_idx, hipStream_t s);
 hipError_t launch_level_histogram(const int32_t* level, int32_t b, int32_t L, int32_t* hist, hipStream_t s);
 
+// ---- merge of shard lists ----
+struct ShardOffsets {
+    int32_t v[APC_MAX_SHARDS];
+};
+hipError_t launch_merge_shards(const float* scores, const int32_t* idx, int32_t g, int32_t b, int32_t kin,
+                               const ShardOffsets& off, int32_t k, float* out_s, int32_t* out_i, hipStream_t s);
+
 // ---- gather ----------------------------------------------------------------
 hipError_t launch_gather(const void* pool, int64_t n_entries, int64_t n_slots, int64_t latent_bytes,
                          const int32_t* slot_of_entry, const int32_t* top_idx, int32_t ld, int32_t b,
