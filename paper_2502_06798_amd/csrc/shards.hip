@@ -19,16 +19,31 @@ __device__ inline uint64_t shard_key(float s, int32_t e)
     return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)e;
 }
 
+// max with the key of the lane a DPP control names (own key where it names
+// none or the row is masked off)
+template <int CTRL, int ROWS>
+__device__ inline uint64_t dpp_max(uint64_t v)
+{
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+    const uint64_t o = ((uint64_t)(uint32_t)__builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xf, false) << 32) |
+                       (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xf, false);
+    return o > v ? o : v;
+}
+
+// largest key of the wavefront: within quads, half rows and rows by
+// permutes and mirrors, then across rows by the broadcasts of lanes 15 and
+// 31; lane 63 ends with the maximum, read back as a scalar
 __device__ inline uint64_t wave_max_u64(uint64_t v)
 {
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
-        const uint64_t o = ((uint64_t)hi << 32) | lo;
-        v = o > v ? o : v;
-    }
-    return v;
+    v = dpp_max<0xB1, 0xf>(v);       // quad_perm [1, 0, 3, 2]
+    v = dpp_max<0x4E, 0xf>(v);       // quad_perm [2, 3, 0, 1]
+    v = dpp_max<0x141, 0xf>(v);      // row_half_mirror
+    v = dpp_max<0x140, 0xf>(v);      // row_mirror
+    v = dpp_max<0x142, 0xa>(v);      // row_bcast:15 into rows 1 and 3
+    v = dpp_max<0x143, 0xc>(v);      // row_bcast:31 into rows 2 and 3
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
 }
 
 __global__ __launch_bounds__(MS_WAVES * 64) void k_merge_shards(const float* __restrict__ sc,
