@@ -283,9 +283,11 @@ apc_status apc_gather_latents_at_level(const apc_cache* c, const int32_t* top_id
                                        void* batch_latents, int32_t* hit, void* stream);
 
 /*
- * Merge of the top-k lists of row shards of one cache (the cache split by
- * rows over g devices: each runs apc_match_batch on its shard, the lists are
- * exchanged, and every device merges them).  scores / idx: g x b x k_in
+ * Merge of the top-k lists of row shards of one cache (not a step of the
+ * paper: the layout for a cache split by rows over g devices, where each runs
+ * apc_match_batch on its shard, the lists are exchanged, and every device
+ * merges them; the paper's nearest-cache retrieval is the whole cache's
+ * top-k, which this reproduces).  scores / idx: g x b x k_in
  * lists as the shards' apc_match_batch calls wrote them (shard s's block at
  * s * b * k_in, best first, entries local to the shard), contiguous as an
  * all-gather leaves them.  offsets (host) g global entry numbers of the

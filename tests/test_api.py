@@ -28,7 +28,9 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for required in ("apc_build_cache", "apc_match_batch", "apc_assign", "apc_gather_latents",
-                     "apc_destroy_cache", "apc_match_workspace", "apc_last_error", "apc_status_str"):
+                     "apc_destroy_cache", "apc_match_workspace", "apc_last_error", "apc_status_str",
+                     "apc_route_plan", "apc_assign_routed", "apc_assign_planned", "apc_resident_best",
+                     "apc_level_histogram", "apc_gather_latents_at_level", "apc_merge_shards"):
         assert required in names
 
 
@@ -99,3 +101,19 @@ def test_match_and_gather_reject_null_handle(lib):
     assert lib.apc_row_factors(9, 4, 16, FAKE, FAKE, None) == E_DTYPE
     assert lib.apc_cache_row_factors(None, FAKE, None) == E_ARG
     lib.apc_destroy_cache(None)
+
+
+def test_merge_shards_argument_checks(lib):
+    import ctypes
+    import numpy as np
+    off = np.zeros(65, dtype=np.int32)
+    fake = ctypes.c_void_p(256)                              # never dereferenced: the checks fail first
+    call = lambda g, b, kin, k, o=off.ctypes.data: lib.apc_merge_shards(fake, fake, g, b, kin, o, k, fake, fake, None)
+    assert call(0, 4, 10, 10) == 1
+    assert call(65, 4, 10, 10) == 1
+    assert call(2, 4, 0, 10) == 1
+    assert call(2, 4, 10, 65) == 1
+    assert call(2, 4, 10, 10, None) == 1
+    neg = np.array([0, -5], dtype=np.int32)
+    assert call(2, 4, 10, 10, neg.ctypes.data) == 1
+    assert call(2, 0, 10, 10) == 0                           # empty batch: nothing to do
