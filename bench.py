@@ -242,7 +242,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="replay one HIP graph per cache copy instead of launching eagerly "
-                         "(measured slower on this stack: 0.131 vs 0.124 ms per step at b256)")
+                         "(measured slower on this stack: 0.104 vs 0.098 ms per step at b256)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain copy of this many MiB (HBM counter calibration)")
     ap.add_argument("--route", choices=("rounds", "planned"), default="rounds",
