@@ -38,7 +38,7 @@ hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, co
 __host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }
 
 // ---- similarity + top-k ----------------------------------------------------
-enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QSTAT = 3, KERNEL_QS = 4 };
+enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QS = 4 };
 struct MatchPlan {
     int kernel;        // kernel variant id
     int bq;            // queries per workgroup tile
@@ -60,14 +60,6 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
 hipError_t launch_stream(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb,
                          const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
                          float* fq, float* ps, int* pi, hipStream_t s);
-
-// query-stationary kernel for small batches of 16-bit or e4m3 rows (k <= 16):
-// queries held in registers, cache rows staged through LDS once per workgroup.
-// qstat_queries gives the queries per workgroup for a row size (0: not built).
-int qstat_queries(int dt, int64_t row_bytes);
-hipError_t launch_qstat(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb,
-                        const float* fe, const void* q, const float* q_scale, int32_t b, int32_t k,
-                        float* fq, float* ps, int* pi, hipStream_t s);
 
 // query-stationary kernel for 16-bit and e4m3 rows of 512, 768, 1024 or 1536 bytes (k <= qs_max_k()):
 // queries in VGPRs, cache rows through an LDS ring, per-query bounds shared

@@ -485,7 +485,6 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
     const int q2b = qs_queries(dt, rb, k);
-    const int qsb = qstat_queries(dt, rb);
     if (q2b > 0 && k <= qs_max_k()) {
         // 16-bit or e4m3 rows: queries in VGPRs, cache rows through LDS, one
         // workgroup per CU; the query tiles of a split share an XCD
@@ -497,19 +496,6 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
         const int64_t ngr = (n + gr - 1) / gr;
         int64_t splits = p.qtiles >= 256 ? 1 : 256 / p.qtiles;
         if (splits > ngr) splits = ngr;
-        if (splits < 1) splits = 1;
-        p.splits = (int)splits;
-    } else if (qsb > 0 && k <= 16 && b <= 2 * qsb) {
-        // small batch, 16-bit or e4m3 rows: queries in registers, each cache row
-        // staged through LDS once per workgroup
-        p.kernel = KERNEL_QSTAT;
-        p.bq = qsb;
-        p.qtiles = (b + p.bq - 1) / p.bq;
-        if (p.qtiles < 1) p.qtiles = 1;
-        const int64_t nblk = (n + 31) / 32;
-        int64_t splits = 256 / p.qtiles;                     // one workgroup per CU
-        if (splits >= 8) splits &= ~(int64_t)7;              // query tiles of a split share an XCD
-        if (splits > nblk) splits = nblk >= 8 ? (nblk & ~(int64_t)7) : nblk;
         if (splits < 1) splits = 1;
         p.splits = (int)splits;
     } else if (b <= 256 && rb <= 3072 && rb % group == 0) {
@@ -576,9 +562,6 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, s)) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qs(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
-    } else if (p.kernel == KERNEL_QSTAT) {
-        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
-        e = launch_qstat(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_stream(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
