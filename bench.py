@@ -100,28 +100,91 @@ def alg_bytes(w):
     return w.N * w.d * eb + 4 * w.N + w.B * (w.d * eb + scale) + 8 * w.B * w.k
 
 
-def cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta, n_queries, min_seconds=10.0):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta, n_queries, min_seconds=10.0, one_thread_queries=2):
     """The float64 reference on the first n_queries queries against the full cache,
-    repeated until at least min_seconds of CPU work have been timed."""
+    repeated until at least min_seconds of CPU work have been timed; then the
+    same on one_thread_queries queries with one thread."""
     from oracle import oracle
     from paper_2502_06798_amd.synth import host_view
     eh, qh = host_view(e), host_view(q[:n_queries])
     esh, qsh = host_view(es), host_view(None if qs is None else qs[:n_queries])
     e_sq, _, _ = oracle.row_sqnorms(w.dtype, eh, esh)
+    threads = oracle.max_threads()
+
+    def one_pass(n, thr):
+        q_sq, _, _ = oracle.row_sqnorms(w.dtype, qh[:n], None if qsh is None else qsh[:n])
+        ts, ti = oracle.topk(w.dtype, qh[:n], None if qsh is None else qsh[:n], eh, esh, w.k,
+                             threads=thr, q_sq=q_sq, e_sq=e_sq)
+        lv = oracle.levels(ts[:, 0], theta)
+        oracle.assign(lv, w.L, lvl, cap, queue)
+
     reps, dt = 0, 0.0
     while dt < min_seconds:
         t0 = time.perf_counter()
-        q_sq, _, _ = oracle.row_sqnorms(w.dtype, qh, qsh)
-        ts, ti = oracle.topk(w.dtype, qh, qsh, eh, esh, w.k, q_sq=q_sq, e_sq=e_sq)
-        lv = oracle.levels(ts[:, 0], theta)
-        oracle.assign(lv, w.L, lvl, cap, queue)
+        one_pass(n_queries, threads)
         dt += time.perf_counter() - t0
         reps += 1
-    return {"value": round(reps * n_queries / dt, 3), "unit": "prompts/s", "cores": oracle.max_threads(),
-            "kind": "oracle",
+    n1 = min(one_thread_queries, n_queries)
+    t0 = time.perf_counter()
+    one_pass(n1, 1)
+    dt1 = time.perf_counter() - t0
+    oracle.topk(w.dtype, qh[:1], None if qsh is None else qsh[:1], eh[:w.k], None if esh is None else esh[:w.k],
+                w.k, threads=threads)                     # restores the thread count for later calls
+    return {"value": round(reps * n_queries / dt, 3), "unit": "prompts/s", "cores": threads,
+            "kind": "oracle", "cpu": cpu_model(), "nproc": os.cpu_count(),
+            "one_thread": {"value": round(n1 / dt1, 4), "unit": "prompts/s", "cores": 1,
+                           "sample": f"{n1} queries, {dt1:.2f} s"},
             "sample": f"{reps} x {n_queries} of {w.B} queries of {w.name} against all {w.N} entries "
-                      f"(top-{w.k}, levels, assignment), {dt:.2f} s; the entry norms are "
-                      "computed once outside the timed part"}
+                      f"(top-{w.k}, levels, assignment), {dt:.2f} s with {threads} threads; the entry "
+                      "norms are computed once outside the timed part"}
+
+
+def gather_rate(apc, step, cache, soe, w, ns):
+    """The latent gather alone on a batch where every placed query's top-1 is
+    resident (the step's own placement, top-1 replaced by resident entries):
+    HBM bytes = each copied latent read once and written once."""
+    import numpy as np
+    import torch
+    if step.batch is None:
+        return None
+    if soe is None:
+        hot = torch.arange(min(w.N, w.B), dtype=torch.int32, device="cuda")
+    else:
+        hot = torch.nonzero(soe >= 0).flatten().to(torch.int32)
+    top = step.top_idx.clone()
+    top[:, 0] = hot[torch.arange(w.B, device="cuda") % hot.numel()]
+    lv = torch.where(step.out_level >= 0, torch.ones_like(step.out_level), step.out_level)
+    hit = torch.empty_like(step.hit)
+    ev = HipEvents(ns)
+    ev.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    cur = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for i in range(ns + 3):
+        if i >= 3:
+            ev.hip.hipEventRecord(ev.pairs[i - 3][0], cur)
+        apc.apc_gather_latents(cache, top, w.k, w.B, lv, step.out_inst, step.out_slot, step.n_inst, step.spi,
+                               step.batch, hit)
+        if i >= 3:
+            ev.hip.hipEventRecord(ev.pairs[i - 3][1], cur)
+    torch.cuda.synchronize()
+    ms = float(np.median([ev.elapsed_ms(i) for i in range(ns)]))
+    ev.close()
+    copies = int(hit.sum().item())
+    nbytes = 2 * copies * w.latent_bytes
+    return {"copies": copies, "latent_bytes": w.latent_bytes, "ms": round(ms, 5), "bytes": nbytes,
+            "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "batch": "the step's placement with every placed query's top-1 resident"}
 
 
 def copy_probe(mib, reps=5):
@@ -235,10 +298,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="b256_n100k_d768_f16")
+    ap.add_argument("--workload", default="b16384_n10m_d768_e4m3",
+                    help="the largest workload that fits one GPU by default; the others are parity cases")
     ap.add_argument("--copies", type=int, default=0, help="cache copies rotated per step (0 = auto)")
-    ap.add_argument("--cpu-queries", type=int, default=256)
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-queries", type=int, default=128,
+                    help="queries of the batch the float64 reference is timed on (all threads)")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--cpu-one-thread-queries", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="replay one HIP graph per cache copy instead of launching eagerly "
@@ -402,6 +468,7 @@ def main():
     torch.cuda.synchronize()
     assign_ms = float(np.median([ev.elapsed_ms(i) for i in range(ns)]))
     ev.close()
+    gather = gather_rate(apc, step, caches[0], soe, w, ns)
     # warm: one cache copy, left in the MALL between steps (only where it fits)
     warm = None
     if copies > 1:
@@ -451,13 +518,15 @@ def main():
         "warm_ms_per_step": warm,
         "assign_ms": round(assign_ms, 5),
         "latent_hit_rate": hit_rate,
+        "gather": gather,
         "overlapped": overlapped,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU reference")
         out["cpu_baseline"] = cpu_baseline(w, e, es, q, qs, lvl, cap, queue, theta,
-                                           min(args.cpu_queries, w.B), args.cpu_seconds)
+                                           min(args.cpu_queries, w.B), args.cpu_seconds,
+                                           args.cpu_one_thread_queries)
     for c in caches:
         c.close()
     print(json.dumps(out), flush=True)

@@ -22,6 +22,9 @@
  *    non-OK status nothing was enqueued and no output was written, except
  *    APC_E_HIP (a launch failed; outputs are unspecified).
  *  - apc_last_error() gives a thread-local message for the last failing call.
+ *  - Calls that take a cache handle must run with the handle's device
+ *    current (the device that was current at apc_build_cache); on another
+ *    device they return APC_E_ARG before enqueuing anything.
  *  - Calls on different streams may run concurrently when they write
  *    disjoint buffers (each match call needs its own workspace).
  */
@@ -253,12 +256,15 @@ apc_status apc_resident_best(const apc_cache* c, const float* top_score, const i
 apc_status apc_level_histogram(const int32_t* level, int32_t b, int32_t L, int32_t* hist, void* stream);
 
 /*
- * Latent gather (the cached intermediate state a placed prompt starts from):
- * for each query with out_level > 0 whose top-1 entry top_idx[q * ld] has a
- * resident latent, copy it to batch_latents[(out_inst * slots_per_inst +
- * out_slot) * latent_bytes] and set hit[q] = 1; otherwise hit[q] = 0 and that
- * batch slot is not written.  out_slot must be < slots_per_inst for every
- * copied query (as apc_assign produces with slots_per_inst >= max capacity).
+ * Latent gather (the cached intermediate state a placed prompt starts from:
+ * the Introduction's reuse of a prior prompt's intermediate state, which
+ * skips K denoising steps, and the Query Dispatcher's route-and-batch, which
+ * hands every worker its batch): for each query with out_level > 0 whose
+ * top-1 entry top_idx[q * ld] has a resident latent, copy it to
+ * batch_latents[(out_inst * slots_per_inst + out_slot) * latent_bytes] and
+ * set hit[q] = 1; otherwise hit[q] = 0 and that batch slot is not written.
+ * out_slot must be < slots_per_inst for every copied query (as apc_assign
+ * produces with slots_per_inst >= max capacity).
  */
 apc_status apc_gather_latents(const apc_cache* c, const int32_t* top_idx, int32_t ld, int32_t b,
                               const int32_t* out_level, const int32_t* out_inst,
@@ -292,12 +298,13 @@ apc_status apc_gather_latents_at_level(const apc_cache* c, const int32_t* top_id
  * s * b * k_in, best first, entries local to the shard), contiguous as an
  * all-gather leaves them.  offsets (host) g global entry numbers of the
  * shards' first rows.  out_score / out_idx: b x k, the best k of all shards'
- * candidates under (score desc, global entry asc); entries < 0 and NaN
- * scores are not candidates, and slots past the last candidate get NaN / -1.
+ * candidates under (score desc, global entry asc); entries < 0, NaN scores
+ * and global entry numbers (entry + offset, summed in 64 bits) of 2^31 - 1
+ * or more are not candidates, and slots past the last candidate get NaN / -1.
  * Since every entry of the whole cache's top-k is in its shard's top-k, the
  * merge of the shards' top-k lists is the whole cache's top-k.
- * 1 <= g <= APC_MAX_SHARDS, 1 <= k, k_in <= APC_MAX_K, offsets >= 0, and the
- * global entry numbers must fit in int32.  Errors: APC_E_ARG.
+ * 1 <= g <= APC_MAX_SHARDS, 1 <= k, k_in <= APC_MAX_K, offsets >= 0.
+ * Errors: APC_E_ARG.
  */
 apc_status apc_merge_shards(const float* scores, const int32_t* idx, int32_t g, int32_t b, int32_t k_in,
                             const int32_t* offsets /* host */, int32_t k, float* out_score, int32_t* out_idx,

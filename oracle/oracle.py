@@ -373,7 +373,9 @@ def gather_at_level(top1, out_level, out_inst, out_slot, slot_of_entry, n_entrie
 def merge_shards(scores, idx, offsets, k: int):
     """scores/idx: (g, b, k_in) lists, best first; offsets: g global offsets.
     Returns (score float32 [b, k], entry int32 [b, k]); slots past the valid
-    candidates (entries < 0 or NaN scores are not candidates) hold NaN / -1."""
+    candidates hold NaN / -1.  Not candidates: entries < 0, NaN scores, and
+    global entry numbers of 2^31 - 1 or more (no cache handle holds that many
+    entries, and the result is int32)."""
     scores = np.asarray(scores, dtype=np.float32)
     idx = np.asarray(idx, dtype=np.int64)
     g, b, kin = idx.shape
@@ -382,7 +384,8 @@ def merge_shards(scores, idx, offsets, k: int):
     for q in range(b):
         cand = [(float(scores[s, q, j]), int(idx[s, q, j]) + int(offsets[s]))
                 for s in range(g) for j in range(kin)
-                if idx[s, q, j] >= 0 and not np.isnan(scores[s, q, j])]
+                if idx[s, q, j] >= 0 and not np.isnan(scores[s, q, j])
+                and int(idx[s, q, j]) + int(offsets[s]) < 2**31 - 1]
         cand.sort(key=lambda c: (-c[0], c[1]))
         for j, (sc, e) in enumerate(cand[:k]):
             out_s[q, j], out_i[q, j] = sc, e

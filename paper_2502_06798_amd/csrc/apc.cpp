@@ -71,6 +71,18 @@ apc_status check_rows(apc_dtype dt, int64_t n, int32_t d, const void* rows, cons
     return APC_OK;
 }
 
+// Calls that take a handle run on the handle's device: its row factors and
+// the caller's borrowed buffers live there.
+apc_status check_device(const char* who, const apc_cache* c)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(APC_E_HIP, "%s: hipGetDevice: %s", who, hipGetErrorString(e));
+    if (dev != c->device)
+        return fail(APC_E_ARG, "%s: the cache was built on device %d but device %d is current", who, c->device, dev);
+    return APC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -208,6 +220,7 @@ void apc_destroy_cache(apc_cache* c)
 apc_status apc_cache_row_factors(const apc_cache* c, float* out, void* stream)
 {
     if (!c || !out) return fail(APC_E_ARG, "apc_cache_row_factors: NULL argument");
+    if (apc_status st = check_device("apc_cache_row_factors", c)) return st;
     hipError_t e = hipMemcpyAsync(out, c->fe, sizeof(float) * c->n, hipMemcpyDeviceToDevice,
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "apc_cache_row_factors");
@@ -234,6 +247,7 @@ apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_sca
     if (b == 0) return ok();
     apc_status st = check_rows(c->dt, b, c->d, q, "apc_match_batch queries");
     if (st != APC_OK) return st;
+    if ((st = check_device("apc_match_batch", c)) != APC_OK) return st;
     if ((c->dt == APC_E4M3) != (q_scale != nullptr))
         return fail(APC_E_ARG, "apc_match_batch: q_scale is required for e4m3 and only for e4m3");
     if (!top_score || !top_idx || !aligned16(top_score) || !aligned16(top_idx))
@@ -412,6 +426,7 @@ apc_status apc_resident_best(const apc_cache* c, const float* top_score, const i
     if (b == 0) return ok();
     if (!top_score || !top_idx || !out_score || !out_idx)
         return fail(APC_E_ARG, "apc_resident_best: NULL device buffer");
+    if (apc_status st = check_device("apc_resident_best", c)) return st;
     hipError_t e = apc::launch_resident_best(c->slot_of_entry, c->n, c->n_slots, top_score, top_idx, ld, k, b,
                                              out_score, out_idx, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "apc_resident_best launch");
@@ -465,6 +480,7 @@ static apc_status gather_impl(const char* who, const apc_cache* c, const int32_t
         return fail(APC_E_ARG, "%s: NULL device buffer", who);
     if ((int64_t)n_inst * slots_per_inst > 0 && (!batch_latents || !aligned16(batch_latents)))
         return fail(APC_E_ARG, "%s: batch_latents must be 16-byte aligned", who);
+    if (apc_status st = check_device(who, c)) return st;
     hipError_t e = apc::launch_gather(c->latents, c->n, c->n_slots, c->latent_bytes, c->slot_of_entry,
                                       top_idx, ld, b, out_level, out_inst, out_slot, n_inst, slots_per_inst, lps,
                                       batch_latents, hit, static_cast<hipStream_t>(stream));

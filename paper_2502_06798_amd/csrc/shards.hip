@@ -66,8 +66,11 @@ __global__ __launch_bounds__(MS_WAVES * 64) void k_merge_shards(const float* __r
         while (lane < g && head < kin) {                      // skip non-candidates
             hs = sc[base + head];
             const int32_t e = ix[base + head];
-            if (e >= 0 && hs == hs) {
-                he = e + o;
+            // the global entry number, in 64 bits: one that does not fit below
+            // 2^31 - 1 (the largest cache a handle takes) is not a candidate
+            const int64_t ge = (int64_t)e + o;
+            if (e >= 0 && hs == hs && ge < INT32_MAX) {
+                he = (int32_t)ge;
                 key = shard_key(hs, he);
                 break;
             }

@@ -144,7 +144,7 @@ def test_match_small(apc, orc, dtype, b, n, d, k):
     torch.cuda.synchronize()
     qh, eh = stored_np(q), stored_np(e)
     qsh, esh = np_or_none(qs), np_or_none(es)
-    rs, ri = orc.topk(dtype, qh, qsh, eh, esh, k)
+    rs, ri = orc.topk(dtype, qh, qsh, eh, esh, min(k + 1, n))
     st = check_topk(orc, dtype, qh, qsh, eh, esh, ts.cpu().numpy(), ti.cpu().numpy(), rs, ri)
     say("  ", st)
     # deterministic: a second run is bit-identical
@@ -175,7 +175,7 @@ def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
     rows = np.arange(0, b, 61)
     qh, eh = stored_np(q), stored_np(e)
     qsh, esh = np_or_none(qs), np_or_none(es)
-    rs, ri = orc.topk(dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, k)
+    rs, ri = orc.topk(dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, k + 1)
     st = check_topk(orc, dtype, qh, qsh, eh, esh, ts.cpu().numpy(), ti.cpu().numpy(), rs, ri, rows=rows)
     say("  ", st)
     c.close()
@@ -243,7 +243,9 @@ def _random_table(rng, L, I, cap_hi=6):
 
 
 @pytest.mark.parametrize("b,L,I", [(1, 0, 1), (16, 5, 2), (64, 3, 3), (65, 5, 4), (200, 5, 4), (256, 5, 4),
-                                    (130, 32, 20), (300, 5, 8), (2500, 10, 40), (5000, 32, 256)])
+                                    (130, 32, 20), (300, 5, 8), (2500, 10, 40), (5000, 32, 256),
+                                    # above 16384 queries: the multi-block placement kernel
+                                    (20000, 10, 32), (20000, 32, 64), (65536, 10, 16), (65536, 32, 256)])
 def test_assign_bit_exact(apc, orc, b, L, I):
     say(f"assign b={b} L={L} I={I}")
     rng = np.random.default_rng(b + L + I)

@@ -82,3 +82,22 @@ def test_sharded_match_equals_whole_cache(apc, dtype, cuts):
     assert torch.equal(mi, ti) and torch.equal(ms, ts)
     for c in caches + [whole]:
         c.close()
+
+
+def test_merge_shards_offsets_near_int32_limit(apc, orc):
+    # global entry numbers are summed in 64 bits; those of 2^31 - 1 or more are
+    # not candidates (they would wrap to negative int32 numbers)
+    say("merge_shards offsets near 2^31")
+    rng = np.random.default_rng(99)
+    g, b, kin, k = 4, 200, 16, 20
+    s, i = _shard_lists(rng, g, b, kin, 500)
+    offsets = [0, 2**31 - 650, 2**31 - 150, 2**31 - 1]   # disjoint ranges; the last two partly or wholly past the limit
+    os_ = torch.full((b, k), 7.0, device="cuda")
+    oi = torch.full((b, k), 7, dtype=torch.int32, device="cuda")
+    apc.apc_merge_shards(torch.from_numpy(s).cuda(), torch.from_numpy(i).cuda(), g, b, kin, offsets, k, os_, oi)
+    torch.cuda.synchronize()
+    ws, wi = orc.merge_shards(s, i, offsets, k)
+    gs = os_.cpu().numpy()
+    assert np.array_equal(oi.cpu().numpy(), wi)
+    assert np.array_equal(np.isnan(gs), np.isnan(ws)) and np.array_equal(gs[~np.isnan(ws)], ws[~np.isnan(ws)])
+    assert (wi >= -1).all() and (wi[:, 0] >= 0).all()

@@ -1,12 +1,18 @@
 """GPU parity on the five synthetic workloads at full size, in the launch
 configuration the benchmark times.
 
-Workloads 1-2: every query is checked against the float64 reference.
-Workloads 3-5: a seeded sample of queries (the reference is brute force over
-all N entries per query).  For every workload the levels of all B queries
-are checked against the reference on the GPU's best scores, the assignment
-is bit-exact given the GPU's levels, and the gathered latents are
-byte-exact given the GPU's top-1 and assignment.
+Workloads 1-3: every query is checked against the float64 reference.
+Workloads 4-5: a structured sample that reaches every 32-query block (the
+unit of a wavefront's queries) and so every query tile and wavefront of the
+similarity kernel: workload 4 takes the first and last row of every block,
+workload 5 one row of every 64 queries, cycling through the first and last
+rows of its two blocks and a seeded random row (the reference is brute force
+over all N entries per query).  Top-k lists are checked with the tolerance
+rule and the strict rule (isolated ranks bit-exact), and the levels of the
+checked rows against the reference's own best.  For every workload the
+levels of all B queries are checked against the reference on the GPU's best
+scores, the assignment is bit-exact given the GPU's levels, and the gathered
+latents are byte-exact given the GPU's top-1 and assignment.
 """
 import gc
 import time
@@ -21,14 +27,18 @@ from tests.gpu_check import TOL, check_levels, check_topk, say
 
 pytestmark = pytest.mark.gpu
 
-SAMPLE = {1: None, 2: None, 3: 48, 4: 24, 5: 12}
 
-
-def _sample_rows(w, n):
-    if n is None or n >= w.B:
+def _sample_rows(w):
+    if w.wid <= 3:
         return np.arange(w.B)
+    if w.wid == 4:
+        blocks = np.arange(0, w.B, 32)
+        return np.unique(np.concatenate([blocks, blocks + 31]))
     rng = np.random.default_rng(synth.seed_of(w.wid, 99))
-    return np.unique(np.concatenate([np.arange(8), rng.choice(w.B, n - 8, replace=False)]))
+    chunks = np.arange(0, w.B, 64)
+    pick = np.array([0, 31, 32, 63])
+    rows = [c + (pick[i % 5] if i % 5 < 4 else rng.integers(0, 64)) for i, c in enumerate(chunks)]
+    return np.unique(np.array(rows))
 
 
 @pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
@@ -64,13 +74,13 @@ def test_workload(orc, wid):
     esh, qsh = np_or_none(es), np_or_none(qs)
 
     # top-k on the checked rows
-    rows = _sample_rows(w, SAMPLE[wid])
+    rows = _sample_rows(w)
     e_sq, rc, _ = orc.row_sqnorms(w.dtype, eh, esh)
     assert rc == 0
     q_sq, rc, _ = orc.row_sqnorms(w.dtype, qh, qsh)
     assert rc == 0
     t1 = time.time()
-    rs, ri = orc.topk(w.dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, w.k,
+    rs, ri = orc.topk(w.dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, w.k + 1,
                       q_sq=q_sq[rows], e_sq=e_sq)
     say(f"  reference top-k of {len(rows)} queries in {time.time() - t1:.1f}s")
     st = check_topk(orc, w.dtype, qh, qsh, eh, esh, ts, ti, rs, ri, rows=rows, q_sq=q_sq, e_sq=e_sq)

@@ -40,3 +40,16 @@ def test_merge_hand_made_lists():
     assert np.allclose(ms, [[0.9, 0.9, 0.7, 0.5, 0.5]])
     ms, mi = oracle.merge_shards(s[:, :, :1] * np.nan, i[:, :, :1], [0, 10, 20], 2)
     assert (mi == -1).all() and np.isnan(ms).all()
+
+
+def test_merge_drops_entries_past_int32():
+    # shard 1 starts 5 entries below 2^31 - 1: its local entries 0..3 fit, 5 and
+    # above would reach 2^31 - 1 or wrap, and are not candidates
+    top = 2**31 - 1
+    s = np.array([[[0.3, 0.2]], [[0.9, 0.8]], [[0.95, 0.1]]], np.float32)
+    i = np.array([[[7, 8]], [[9, 3]], [[0, 1]]])
+    ms, mi = oracle.merge_shards(s, i, [0, top - 5, top - 1], 6)
+    # kept: 0.95 at top - 1, 0.8 at top - 2, 0.3 at 7, 0.2 at 8; dropped: 0.9 at
+    # top + 4 and 0.1 at top
+    assert mi.tolist() == [[top - 1, top - 2, 7, 8, -1, -1]]
+    assert np.allclose(ms[0, :4], [0.95, 0.8, 0.3, 0.2]) and np.isnan(ms[0, 4:]).all()
