@@ -15,12 +15,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libapc.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "assign.hip", "gather.hip", "resident.hip", "shards.hip"]
+SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "qs8_f16.hip", "qs8_bf16.hip", "qs8_e4m3.hip", "assign.hip", "gather.hip", "resident.hip", "shards.hip"]
 
 # Kernels in these sources load into LDS with asm and wait for those loads by
 # counting vector-memory operations themselves; a register spill would add
 # scratch loads to the count, so their code must not use scratch memory.
-COUNTED = ["qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip"]
+COUNTED = ["qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "qs8_f16.hip", "qs8_bf16.hip", "qs8_e4m3.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -32,7 +32,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
 # as separate registers: promoted to one vector, a list is copied whole on
 # every pass of the insertion loop.
 SOURCE_FLAGS = {src: ["-mllvm", "-disable-promote-alloca-to-vector"]
-                for src in ("qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip")}
+                for src in ("qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "qs8_f16.hip", "qs8_bf16.hip", "qs8_e4m3.hip")}
 
 
 def _compile(src: str) -> str:

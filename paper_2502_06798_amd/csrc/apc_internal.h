@@ -38,7 +38,7 @@ hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, co
 __host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }
 
 // ---- similarity + top-k ----------------------------------------------------
-enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QS = 4 };
+enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QS = 4, KERNEL_QS8 = 5 };
 struct MatchPlan {
     int kernel;        // kernel variant id
     int bq;            // queries per workgroup tile
@@ -69,14 +69,21 @@ int qs_max_k();
 // entries per group (the unit a split is made of) of the shape qs_queries describes
 int qs_group_rows(int64_t row_bytes, int k);
 // query factors into fq and reset bounds gthr, for b_pad rows (rows >= b get NaN)
-// query factors and bound reset for the query-stationary kernel; qperm
+// query factors and bound reset for the query-stationary kernels; qperm
 // (b_pad x row_bytes bytes) receives the queries in the order that kernel's
-// lanes load them, for query tiles of bq rows
+// lanes load them, for query tiles of bq rows over nw wavefronts
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, uint8_t* qperm, int bq, hipStream_t s);
+                        float* fq, int* gthr, uint8_t* qperm, int bq, int nw, hipStream_t s);
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
                      hipStream_t s);
+// the same with two wavefronts per SIMD and the top-k lists in LDS, for
+// 16-bit and e4m3 rows of 512 or 768 bytes (k <= 32): qs8_queries gives the
+// queries per workgroup (0: not built), qs8_group_rows the rows per group
+int qs8_queries(int dt, int64_t row_bytes, int k);
+int qs8_group_rows();
+hipError_t launch_qs8(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
+                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

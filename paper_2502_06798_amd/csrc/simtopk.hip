@@ -485,7 +485,19 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     const int64_t group = dt == APC_E4M3 ? 6 * 128 : 4 * 128;   // chunks in flight x 128 bytes
     const int q2b = qs_queries(dt, rb, k);
-    if (q2b > 0 && k <= qs_max_k()) {
+    const int q8b = qs8_queries(dt, rb, k);
+    if (q8b > 0 && b > 256) {
+        // large batches of 512- or 768-byte rows: two wavefronts per SIMD,
+        // 256 queries per workgroup, one workgroup per CU
+        p.kernel = KERNEL_QS8;
+        p.bq = q8b;
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        const int64_t ngr = (n + qs8_group_rows() - 1) / qs8_group_rows();
+        int64_t splits = p.qtiles >= 256 ? 1 : 256 / p.qtiles;
+        if (splits > ngr) splits = ngr;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+    } else if (q2b > 0 && k <= qs_max_k()) {
         // 16-bit or e4m3 rows: queries in VGPRs, cache rows through LDS, one
         // workgroup per CU; the query tiles of a split share an XCD
         p.kernel = KERNEL_QS;
@@ -530,7 +542,8 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     p.off_ps = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
     p.off_qp = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
-    const size_t qp_bytes = p.kernel == KERNEL_QS ? (size_t)p.b_pad * (size_t)d * elem_bytes(dt) : 0;
+    const size_t qp_bytes =
+        p.kernel == KERNEL_QS || p.kernel == KERNEL_QS8 ? (size_t)p.b_pad * (size_t)d * elem_bytes(dt) : 0;
     p.bytes = align256(p.off_qp + qp_bytes);
     return p;
 }
@@ -559,9 +572,15 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
         uint8_t* qp = w + p.off_qp;
-        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, s)) != hipSuccess) return e;
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 4, s)) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qs(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
+    } else if (p.kernel == KERNEL_QS8) {
+        int* gt = reinterpret_cast<int*>(w + p.off_gt);
+        uint8_t* qp = w + p.off_qp;
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 8, s)) != hipSuccess) return e;
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        e = launch_qs8(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_stream(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);

@@ -181,6 +181,50 @@ def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
     c.close()
 
 
+# Batches above 256 queries with 512- or 768-byte rows go to the kernel with
+# two wavefronts per SIMD (256 queries per workgroup, lists in LDS): every row
+# type, both list sizes (k <= 16 and k <= 32), k = 1 and k = 32, a last group
+# of fewer than 64 rows, a cache smaller than one group, wavefronts without
+# queries (b just above a multiple of 32 and of 256) and many splits.
+QS8_CASES = [
+    ("e4m3", 257, 5000, 768, 10),
+    ("e4m3", 300, 63, 512, 32),        # fewer rows than one group
+    ("e4m3", 1000, 20011, 512, 1),
+    ("f16", 513, 9000, 384, 16),       # 768-byte f16 rows
+    ("bf16", 700, 12345, 256, 17),     # 512-byte bf16 rows, 32-slot lists
+    ("f16", 2080, 30001, 256, 32),
+    ("bf16", 1024, 7000, 384, 5),
+    ("e4m3", 4099, 40000, 768, 32),
+]
+
+
+@pytest.mark.parametrize("dtype,b,n,d,k", QS8_CASES)
+def test_match_two_waves_per_simd(apc, orc, dtype, b, n, d, k):
+    say(f"match (two wavefronts per SIMD) {dtype} b={b} n={n} d={d} k={k}")
+    e, es = make_rows(n, d, dtype, 50 + n, clusters=max(1, n // 60))
+    q, qs = make_rows(b, d, dtype, 60 + b, clusters=None)
+    q[: b // 2] = e[torch.arange(b // 2, device="cuda") * 11 % n]
+    if qs is not None:
+        qs[: b // 2] = es[torch.arange(b // 2, device="cuda") * 11 % n]
+    c = apc.apc_build_cache(e, es)
+    ts = torch.empty((b, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((b, k), dtype=torch.int32, device="cuda")
+    ws = apc.workspace_tensor(c, b, k)
+    apc.apc_match_batch(c, q, qs, k, ts, ti, ws)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(0, b, max(1, b // 160)), [b - 1], np.arange(min(b, 40))]))
+    qh, eh = stored_np(q), stored_np(e)
+    qsh, esh = np_or_none(qs), np_or_none(es)
+    rs, ri = orc.topk(dtype, qh[rows], None if qsh is None else qsh[rows], eh, esh, min(k + 1, n))
+    st = check_topk(orc, dtype, qh, qsh, eh, esh, ts.cpu().numpy(), ti.cpu().numpy(), rs, ri, rows=rows)
+    say("  ", st)
+    ts2, ti2 = torch.empty_like(ts), torch.empty_like(ti)
+    apc.apc_match_batch(c, q, qs, k, ts2, ti2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(ti, ti2) and torch.equal(ts, ts2)
+    c.close()
+
+
 def test_match_ties_take_lower_index(apc, orc):
     say("match ties")
     row = torch.randn(1, 64, device="cuda").half()
