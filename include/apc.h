@@ -134,6 +134,23 @@ apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_sca
                            size_t ws_bytes, void* stream);
 
 /*
+ * apc_match_batch without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the workspace is a static device array
+ * of APC_STATIC_WS_BYTES that each device holds from the library's first
+ * use on it until the process ends (looked up on the first call on a
+ * device).  The call allocates nothing.  Same arguments, outputs and errors
+ * as apc_match_batch, plus APC_E_WORKSPACE when apc_match_workspace(c, b, k)
+ * exceeds APC_STATIC_WS_BYTES (every workload up to 16,384 queries x k = 32
+ * fits).  Nothing in the array needs to start at zero.  All calls on one
+ * device share the array: calls that overlap on one device (other streams,
+ * other threads) race and give undefined results; serialise them.
+ */
+#define APC_STATIC_WS_BYTES (32u << 20)
+apc_status apc_match_batch_static(const apc_cache* c, const void* q, const float* q_scale, int32_t b,
+                                  int32_t k, float* top_score, int32_t* top_idx, void* stream);
+
+/*
  * Optimal level and capacity-constrained placement (Approach: optimal-K,
  * redirection to K' < K or to the closest K' > K with Eq. 1 charging
  * degradation only upwards; greedy route-and-batch filling the longest

@@ -12,7 +12,7 @@ from .binding import (APC_BF16, APC_E4M3, APC_F16, APC_F32, APC_MAX_INST, APC_MA
                       apc_assign_routed, apc_build_cache,
                       apc_cache_row_factors, apc_destroy_cache, apc_gather_latents,
                       apc_gather_latents_at_level,
-                      apc_last_error, apc_level_histogram, apc_match_batch, apc_match_workspace,
+                      apc_last_error, apc_level_histogram, apc_match_batch, apc_match_batch_static, apc_match_workspace,
                       apc_merge_shards, apc_resident_best, apc_route_plan,
                       apc_row_factors, apc_set_kernel_events, apc_status_str, load, workspace_tensor)
 from .pipeline import MatchStep
@@ -22,7 +22,7 @@ __all__ = ["APC_BF16", "APC_E4M3", "APC_F16", "APC_F32", "APC_MAX_INST", "APC_MA
            "apc_assign_routed", "apc_build_cache",
            "apc_cache_row_factors", "apc_destroy_cache", "apc_gather_latents",
            "apc_gather_latents_at_level", "apc_last_error",
-           "apc_level_histogram", "apc_match_batch", "apc_match_workspace", "apc_merge_shards", "apc_resident_best",
+           "apc_level_histogram", "apc_match_batch", "apc_match_batch_static", "apc_match_workspace", "apc_merge_shards", "apc_resident_best",
            "apc_route_plan", "apc_row_factors", "apc_set_kernel_events",
            "apc_status_str", "load",
            "workspace_tensor"]

@@ -60,6 +60,8 @@ def load() -> ctypes.CDLL:
     L.apc_match_workspace.restype = st
     L.apc_match_batch.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp, sz, vp]
     L.apc_match_batch.restype = st
+    L.apc_match_batch_static.argtypes = [vp, vp, vp, i32, i32, vp, vp, vp]
+    L.apc_match_batch_static.restype = st
     L.apc_assign.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.apc_assign.restype = st
     L.apc_route_plan.argtypes = [i32, vp, vp, vp, vp, ctypes.POINTER(i64)]
@@ -201,6 +203,14 @@ def apc_match_batch(c: Cache, q: torch.Tensor, q_scale: Optional[torch.Tensor], 
     _check(load().apc_match_batch(c.handle, _ptr(q), _ptr(q_scale), b, k, _ptr(top_score),
                                   _ptr(top_idx), _ptr(ws), ws.numel() * ws.element_size(),
                                   _stream(stream)))
+
+
+def apc_match_batch_static(c: Cache, q: torch.Tensor, q_scale: Optional[torch.Tensor], k: int,
+                           top_score: torch.Tensor, top_idx: torch.Tensor, stream=None):
+    """apc_match_batch on the library's static device workspace (allocates nothing)."""
+    b = q.shape[0]
+    _check(load().apc_match_batch_static(c.handle, _ptr(q), _ptr(q_scale), b, k, _ptr(top_score),
+                                         _ptr(top_idx), _stream(stream)))
 
 
 def apc_assign(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float], K: Sequence[int],

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <climits>
 #include <cmath>
@@ -28,7 +29,15 @@ struct apc_cache {
     int device;
 };
 
+// Workspace of apc_match_batch_static: one copy per device, held until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address (per device) comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[APC_STATIC_WS_BYTES];
+
 namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::atomic<void*> g_scratch_ptr[MAX_DEVICES];   // device address of `scratch` per device (null: not looked up yet)
 
 thread_local std::string g_err;
 thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
@@ -261,6 +270,46 @@ apc_status apc_match_batch(const apc_cache* c, const void* q, const float* q_sca
     hipError_t e = apc::launch_match(p, c->dt, c->n, c->d, c->emb, c->fe, q, q_scale, b, k, top_score,
                                      top_idx, ws, static_cast<hipStream_t>(stream), ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "apc_match_batch launch");
+    return ok();
+}
+
+apc_status apc_match_batch_static(const apc_cache* c, const void* q, const float* q_scale, int32_t b, int32_t k,
+                                  float* top_score, int32_t* top_idx, void* stream)
+{
+    if (!c) return fail(APC_E_ARG, "apc_match_batch_static: NULL cache");
+    if (b < 0) return fail(APC_E_ARG, "apc_match_batch_static: b < 0");
+    if (k < 1 || k > APC_MAX_K || k > c->n)
+        return fail(APC_E_ARG, "apc_match_batch_static: need 1 <= k <= min(n, %d) (k=%d)", APC_MAX_K, k);
+    if (b == 0) return ok();
+    apc_status st = check_rows(c->dt, b, c->d, q, "apc_match_batch_static queries");
+    if (st != APC_OK) return st;
+    if ((st = check_device("apc_match_batch_static", c)) != APC_OK) return st;
+    if ((c->dt == APC_E4M3) != (q_scale != nullptr))
+        return fail(APC_E_ARG, "apc_match_batch_static: q_scale is required for e4m3 and only for e4m3");
+    if (!top_score || !top_idx || !aligned16(top_score) || !aligned16(top_idx))
+        return fail(APC_E_ARG, "apc_match_batch_static: outputs must be 16-byte aligned device pointers");
+    const apc::MatchPlan p = apc::plan_match(c->dt, c->n, c->d, b, k);
+    if (p.bytes > (size_t)APC_STATIC_WS_BYTES)
+        return fail(APC_E_WORKSPACE,
+                    "apc_match_batch_static: b = %d, k = %d needs %zu workspace bytes, more than the %u of the "
+                    "static workspace (use apc_match_batch with a workspace of apc_match_workspace() bytes)",
+                    b, k, p.bytes, (unsigned)APC_STATIC_WS_BYTES);
+    if (c->device < 0 || c->device >= MAX_DEVICES)
+        return fail(APC_E_ARG, "apc_match_batch_static: device %d beyond the %d this library tracks", c->device,
+                    MAX_DEVICES);
+    void* ws = g_scratch_ptr[c->device].load(std::memory_order_acquire);
+    if (!ws) {
+        // first call on this device (the handle's device is current): the
+        // device's own copy of the array
+        hipError_t e = hipGetSymbolAddress(&ws, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ws) return hip_fail(e, "apc_match_batch_static: hipGetSymbolAddress");
+        g_scratch_ptr[c->device].store(ws, std::memory_order_release);
+    }
+    hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
+    g_ev_start = g_ev_stop = nullptr;
+    hipError_t e = apc::launch_match(p, c->dt, c->n, c->d, c->emb, c->fe, q, q_scale, b, k, top_score, top_idx, ws,
+                                     static_cast<hipStream_t>(stream), ev0, ev1);
+    if (e != hipSuccess) return hip_fail(e, "apc_match_batch_static launch");
     return ok();
 }
 
