@@ -153,6 +153,35 @@ def assign(level: np.ndarray, L: int, inst_level, inst_cap, inst_queue=None):
     return ol, oi, os_, fill
 
 
+# ---- Load-aware route-and-batch (the Query Dispatcher's routing) ------------
+# Reading of the Approach's Query Dispatcher paragraph: the dispatcher routes
+# by load.  At or above the load threshold it routes greedily: the instances
+# of a level are filled longest queue first, each up to its capacity (its
+# optimal batch), which is the placement `assign` computes.  Below the
+# threshold routing is uniform at batch size 1: every instance of a level
+# takes at most one query, and the level's admitted queries go to its
+# instances in the order of caller-drawn random keys (ascending, then
+# instance index), so that with keys drawn uniformly at random each admitted
+# query lands on a uniformly random instance of its level, one per instance.
+# Levels and redirections between levels are those of `assign` in both modes.
+def assign_load_aware(level, L: int, inst_level, inst_cap, inst_queue, inst_rand, load: int, threshold: int):
+    """(routing, out_level, out_inst, out_slot, inst_fill); routing 1 = greedy, 0 = uniform."""
+    if load >= threshold:
+        return (1,) + tuple(assign(level, L, inst_level, inst_cap, inst_queue))
+    il = np.asarray(inst_level, dtype=np.int64)
+    ic = np.asarray(inst_cap, dtype=np.int64)
+    rnd = np.asarray(inst_rand, dtype=np.uint64)
+    n = il.size
+    batch1 = np.minimum(ic, 1).astype(np.int32)                 # batch size 1
+    order = sorted(range(n), key=lambda i: (int(rnd[i]), i))      # the random order of the instances
+    # `assign` fills a level's instances by (queue desc, index asc): queue
+    # lengths n, n - 1, ... in the random order make it fill in that order
+    queue = np.empty(n, dtype=np.int32)
+    for pos, i in enumerate(order):
+        queue[i] = n - pos
+    return (0,) + tuple(assign(level, L, il.astype(np.int32), batch1, queue))
+
+
 def gather(top1, out_level, out_inst, out_slot, slot_of_entry, n_entries, pool: np.ndarray,
            n_inst: int, slots_per_inst: int, batch: np.ndarray):
     """Copies into `batch` (uint8 [n_inst*slots_per_inst, latent_bytes]) in place; returns hit."""
