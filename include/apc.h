@@ -181,6 +181,35 @@ apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L,
                       int32_t* inst_fill, void* stream);
 
 /*
+ * Load-aware route-and-batch (Approach, Query Dispatcher: uniform routing at
+ * batch size 1 under low load, greedy routing to the workers with the
+ * longest queues at their optimal batch size under high load).  Levels and
+ * redirections as for apc_assign; only the routing inside a level changes.
+ *
+ * load, load_threshold (host): the caller's load measure (for example
+ *             queued prompts) and the switch point.  load >= load_threshold:
+ *             greedy routing, exactly apc_assign.  Below it: uniform routing:
+ *             each instance takes at most one query, and a level's admitted
+ *             queries (admission rank t = 0, 1, ..) go to its instances
+ *             ordered by (inst_rand asc, index asc).
+ * inst_rand   (host, n_inst uint32; may be NULL under greedy routing) random
+ *             keys drawn by the caller for this batch: drawn uniformly at
+ *             random, they make each admitted query land on a uniformly
+ *             random instance of its level, one query per instance.
+ * routing     (host, out) 1 = greedy, 0 = uniform.
+ * Other arguments, outputs and errors as for apc_assign; APC_E_ARG when
+ * uniform routing is chosen without inst_rand or routing is NULL.
+ */
+apc_status apc_assign_load_aware(const float* top_score, int32_t ld, int32_t b, int32_t L,
+                                 const float* theta /* host */, const int32_t* K /* host */, int32_t n_inst,
+                                 const int32_t* inst_level /* host */, const int32_t* inst_cap /* host */,
+                                 const int32_t* inst_queue /* host, nullable */,
+                                 const uint32_t* inst_rand /* host, nullable under greedy routing */,
+                                 int64_t load, int64_t load_threshold, int32_t* routing /* host, out */,
+                                 int32_t* opt_level, int32_t* out_level, int32_t* out_inst, int32_t* out_slot,
+                                 int32_t* inst_fill, void* stream);
+
+/*
  * Route-Plan (Eq. 1; the K-to-K' Route Planner of the Resource Controller):
  * an optimal integer plan X for serving per-level demand H with per-level
  * places F.  Host only: no GPU, no stream.

@@ -8,7 +8,7 @@ C ABI of include/apc.h; this package is its thin Python binding plus the
 seeded synthetic workload generator (synth).
 """
 from .binding import (APC_BF16, APC_E4M3, APC_F16, APC_F32, APC_MAX_INST, APC_MAX_K,
-                      APC_MAX_LEVELS, ApcError, Cache, apc_assign, apc_assign_planned,
+                      APC_MAX_LEVELS, ApcError, Cache, apc_assign, apc_assign_load_aware, apc_assign_planned,
                       apc_assign_routed, apc_build_cache,
                       apc_cache_row_factors, apc_destroy_cache, apc_gather_latents,
                       apc_gather_latents_at_level,
@@ -18,7 +18,8 @@ from .binding import (APC_BF16, APC_E4M3, APC_F16, APC_F32, APC_MAX_INST, APC_MA
 from .pipeline import MatchStep
 
 __all__ = ["APC_BF16", "APC_E4M3", "APC_F16", "APC_F32", "APC_MAX_INST", "APC_MAX_K",
-           "APC_MAX_LEVELS", "ApcError", "Cache", "MatchStep", "apc_assign", "apc_assign_planned",
+           "APC_MAX_LEVELS", "ApcError", "Cache", "MatchStep", "apc_assign", "apc_assign_load_aware",
+           "apc_assign_planned",
            "apc_assign_routed", "apc_build_cache",
            "apc_cache_row_factors", "apc_destroy_cache", "apc_gather_latents",
            "apc_gather_latents_at_level", "apc_last_error",

@@ -64,6 +64,9 @@ def load() -> ctypes.CDLL:
     L.apc_match_batch_static.restype = st
     L.apc_assign.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.apc_assign.restype = st
+    L.apc_assign_load_aware.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, i64, i64, vp, vp, vp, vp,
+                                        vp, vp, vp]
+    L.apc_assign_load_aware.restype = st
     L.apc_route_plan.argtypes = [i32, vp, vp, vp, vp, ctypes.POINTER(i64)]
     L.apc_route_plan.restype = st
     L.apc_assign_routed.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -225,6 +228,27 @@ def apc_assign(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float],
     _check(load().apc_assign(_ptr(top_score), ld, b, th.size, _hp(th), _hp(Kh), il.size, _hp(il),
                              _hp(ic), _hp(iq), _ptr(opt_level), _ptr(out_level), _ptr(out_inst),
                              _ptr(out_slot), _ptr(inst_fill), _stream(stream)))
+
+
+def apc_assign_load_aware(top_score: torch.Tensor, ld: int, b: int, theta: Sequence[float], K: Sequence[int],
+                          inst_level: Sequence[int], inst_cap: Sequence[int], inst_queue: Optional[Sequence[int]],
+                          inst_rand: Optional[Sequence[int]], load_value: int, load_threshold: int,
+                          opt_level: torch.Tensor, out_level: torch.Tensor, out_inst: torch.Tensor,
+                          out_slot: torch.Tensor, inst_fill: torch.Tensor, stream=None) -> int:
+    """load_value: the caller's load measure (the C call's `load`).  Returns the
+    routing used: 1 greedy, 0 uniform."""
+    th = _host(theta, np.float32)
+    Kh = _host(K, np.int32)
+    il = _host(inst_level, np.int32)
+    ic = _host(inst_cap, np.int32)
+    iq = _host(inst_queue, np.int32)
+    ir = _host(inst_rand, np.uint32)
+    routing = ctypes.c_int32(-1)
+    _check(load().apc_assign_load_aware(_ptr(top_score), ld, b, th.size, _hp(th), _hp(Kh), il.size, _hp(il),
+                                        _hp(ic), _hp(iq), _hp(ir), int(load_value), int(load_threshold),
+                                        ctypes.byref(routing), _ptr(opt_level), _ptr(out_level), _ptr(out_inst),
+                                        _ptr(out_slot), _ptr(inst_fill), _stream(stream)))
+    return routing.value
 
 
 def apc_route_plan(K: Sequence[int], H: Sequence[int], F: Sequence[int]):

@@ -318,11 +318,13 @@ namespace {
 // Checks the level and instance tables shared by the assignment entry points
 // and builds the device table (levels, instances ordered by (level, queue
 // desc, index asc), places per level).
+// With inst_rand (uniform routing at batch size 1), instances are ordered by
+// (level, inst_rand asc, index asc) and each takes at most one query.
 apc_status build_assign_table(const char* who, const float* top_score, int32_t ld, int32_t b, int32_t L,
                               const float* theta, const int32_t* K, int32_t n_inst, const int32_t* inst_level,
                               const int32_t* inst_cap, const int32_t* inst_queue, const int32_t* opt_level,
                               const int32_t* out_level, const int32_t* out_inst, const int32_t* out_slot,
-                              const int32_t* inst_fill, apc::AssignTable& t)
+                              const int32_t* inst_fill, apc::AssignTable& t, const uint32_t* inst_rand = nullptr)
 {
     if (b < 0 || ld < 1) return fail(APC_E_ARG, "%s: need b >= 0 and ld >= 1", who);
     if (L < 0 || L > APC_MAX_LEVELS) return fail(APC_E_TABLE, "%s: need 0 <= L <= %d", who, APC_MAX_LEVELS);
@@ -359,20 +361,25 @@ apc_status build_assign_table(const char* who, const float* top_score, int32_t l
     int order[APC_MAX_INST];
     for (int i = 0; i < n_inst; ++i) order[i] = i;
     std::stable_sort(order, order + n_inst, [&](int a, int c) {
-        const int qa = inst_queue ? inst_queue[a] : 0, qc = inst_queue ? inst_queue[c] : 0;
         if (inst_level[a] != inst_level[c]) return inst_level[a] < inst_level[c];
+        if (inst_rand) {
+            if (inst_rand[a] != inst_rand[c]) return inst_rand[a] < inst_rand[c];
+            return a < c;
+        }
+        const int qa = inst_queue ? inst_queue[a] : 0, qc = inst_queue ? inst_queue[c] : 0;
         if (qa != qc) return qa > qc;
         return a < c;
     });
+    auto cap_of = [&](int i) { return inst_rand ? std::min(inst_cap[i], 1) : inst_cap[i]; };
     int j = 0;
     for (int p = 0; p <= L; ++p) {
         t.level_first[p] = j;
         int64_t cum = 0;
         while (j < n_inst && inst_level[order[j]] == p) {
             t.ord_inst[j] = (int16_t)order[j];
-            t.ord_cap[j] = inst_cap[order[j]];
+            t.ord_cap[j] = cap_of(order[j]);
             t.ord_cum[j] = (int32_t)cum;
-            cum += inst_cap[order[j]];
+            cum += cap_of(order[j]);
             ++j;
         }
         t.level_cap[p] = (int32_t)cum;
@@ -396,6 +403,30 @@ apc_status apc_assign(const float* top_score, int32_t ld, int32_t b, int32_t L, 
     hipError_t e = apc::launch_assign(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot,
                                       inst_fill, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "apc_assign launch");
+    return ok();
+}
+
+apc_status apc_assign_load_aware(const float* top_score, int32_t ld, int32_t b, int32_t L, const float* theta,
+                                 const int32_t* K, int32_t n_inst, const int32_t* inst_level,
+                                 const int32_t* inst_cap, const int32_t* inst_queue, const uint32_t* inst_rand,
+                                 int64_t load, int64_t load_threshold, int32_t* routing, int32_t* opt_level,
+                                 int32_t* out_level, int32_t* out_inst, int32_t* out_slot, int32_t* inst_fill,
+                                 void* stream)
+{
+    if (!routing) return fail(APC_E_ARG, "apc_assign_load_aware: routing is NULL");
+    const bool greedy = load >= load_threshold;
+    if (!greedy && n_inst > 0 && !inst_rand)
+        return fail(APC_E_ARG, "apc_assign_load_aware: uniform routing needs inst_rand");
+    apc::AssignTable t;
+    apc_status st = build_assign_table("apc_assign_load_aware", top_score, ld, b, L, theta, K, n_inst, inst_level,
+                                       inst_cap, inst_queue, opt_level, out_level, out_inst, out_slot, inst_fill, t,
+                                       greedy ? nullptr : inst_rand);
+    if (st != APC_OK) return st;
+    *routing = greedy ? 1 : 0;
+    if (b == 0 && n_inst == 0) return ok();
+    hipError_t e = apc::launch_assign(t, top_score, ld, b, opt_level, out_level, out_inst, out_slot, inst_fill,
+                                      static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "apc_assign_load_aware launch");
     return ok();
 }
 

@@ -117,3 +117,23 @@ def test_merge_shards_argument_checks(lib):
     neg = np.array([0, -5], dtype=np.int32)
     assert call(2, 4, 10, 10, neg.ctypes.data) == 1
     assert call(2, 0, 10, 10) == 0                           # empty batch: nothing to do
+
+
+def test_load_aware_argument_errors(lib):
+    th = np.array([0.5, 0.7], np.float32)
+    Kh = np.array([5, 10], np.int32)
+    il = np.array([0, 1], np.int32)
+    ic = np.array([1, 1], np.int32)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    routing = ctypes.c_int32(-1)
+    # uniform routing (load below the threshold) without random keys
+    assert lib.apc_assign_load_aware(FAKE, 1, 4, 2, p(th), p(Kh), 2, p(il), p(ic), None, None, 0, 1,
+                                     ctypes.byref(routing), FAKE, FAKE, FAKE, FAKE, FAKE, None) == E_ARG
+    # no place for the routing decision
+    rnd = np.array([3, 1], np.uint32)
+    assert lib.apc_assign_load_aware(FAKE, 1, 4, 2, p(th), p(Kh), 2, p(il), p(ic), None, p(rnd), 0, 1,
+                                     None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E_ARG
+    # table errors are those of apc_assign
+    bad = np.array([0, 3], np.int32)
+    assert lib.apc_assign_load_aware(FAKE, 1, 4, 2, p(th), p(Kh), 2, p(bad), p(ic), None, p(rnd), 5, 1,
+                                     ctypes.byref(routing), FAKE, FAKE, FAKE, FAKE, FAKE, None) == E_TABLE
