@@ -43,7 +43,9 @@ typedef enum {
     APC_F32 = 0,   /* IEEE binary32 */
     APC_F16 = 1,   /* IEEE binary16 */
     APC_BF16 = 2,  /* bfloat16 */
-    APC_E4M3 = 3   /* OCP e4m3fn codes with one float32 scale per row */
+    APC_E4M3 = 3,  /* OCP e4m3fn codes with one float32 scale per row */
+    APC_DTYPE_INT32 = 0x7fffffff  /* not a type: makes every int32 value a valid apc_dtype,
+                                     so unknown types are reported as APC_E_DTYPE */
 } apc_dtype;
 
 typedef enum {
@@ -55,7 +57,9 @@ typedef enum {
     APC_E_ZERO_NORM = 5,  /* a cache row has zero norm */
     APC_E_WORKSPACE = 6,  /* workspace smaller than apc_match_workspace() asks */
     APC_E_NOMEM = 7,      /* device or host allocation failed */
-    APC_E_HIP = 8         /* a HIP runtime call or kernel launch failed */
+    APC_E_HIP = 8,        /* a HIP runtime call or kernel launch failed */
+    APC_STATUS_INT32 = 0x7fffffff  /* not a status: makes every int32 value a valid apc_status,
+                                      so apc_status_str may be given any value */
 } apc_status;
 
 #define APC_MAX_K 64          /* largest neighbour count per query */

@@ -23,8 +23,20 @@ DT = {"f32": 0, "f16": 1, "bf16": 2, "e4m3": 3}
 OK, E_ARG, E_NONFINITE, E_ZERO_NORM, E_NOMEM = 0, 1, 2, 3, 4
 
 
-def build() -> str:
-    """Compile the reference with gcc (OpenMP, no HIP)."""
+CLANG = "/opt/rocm/lib/llvm/bin/clang"
+
+
+def build(sanitize_dir: str = "") -> str:
+    """Compile the reference with gcc (OpenMP, no HIP).  With sanitize_dir, a
+    copy instrumented by AddressSanitizer and UndefinedBehaviorSanitizer
+    instead (clang, against its shared sanitizer runtime), written there."""
+    if sanitize_dir:
+        out = os.path.join(sanitize_dir, "liboracle.so")
+        cmd = [CLANG, "-O1", "-g", "-fno-omit-frame-pointer", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+               "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libasan",
+               "-o", out, SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        return out
     cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
            "-o", LIB, SRC, "-lm"]
     subprocess.run(cmd, check=True)
@@ -35,11 +47,16 @@ _lib = None
 
 
 def lib():
+    """The reference library: liboracle.so beside this file, or the build
+    APC_ORACLE_LIB names (the sanitizer test runs the suite on such a copy)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
-            build()
-        L = ctypes.CDLL(LIB)
+        path = os.environ.get("APC_ORACLE_LIB", "")
+        if not path:
+            path = LIB
+            if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+                build()
+        L = ctypes.CDLL(path)
         vp, i64, i32, dp = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
         L.oracle_decode.argtypes = [ctypes.c_int, vp, vp, i64, i32, dp]
         L.oracle_row_sqnorms.argtypes = [ctypes.c_int, vp, vp, i64, i32, dp, vp]

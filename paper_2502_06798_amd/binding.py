@@ -37,14 +37,16 @@ _lib = None
 
 
 def load() -> ctypes.CDLL:
-    """Load libapc.so; raises if it has not been built."""
+    """Load libapc.so (or the build APC_LIB names, e.g. one whose host code is
+    instrumented by sanitizers); raises if it has not been built."""
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with "
+    path = os.environ.get("APC_LIB", "") or LIB_PATH
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with "
                           "`python -m paper_2502_06798_amd.build_lib` (hipcc, gfx950)")
-    L = ctypes.CDLL(LIB_PATH)
+    L = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     st = ctypes.c_int
     L.apc_build_cache.argtypes = [ctypes.c_int, i64, i32, vp, vp, vp, i64, i64, vp, vp,

@@ -76,6 +76,33 @@ def build(verbose: bool = False) -> str:
     return OUT
 
 
+# Host code of the library (argument checks, tables, the host planner) under
+# AddressSanitizer and UndefinedBehaviorSanitizer: apc.cpp compiled with the
+# sanitizers on its host side only, linked with the other objects of the
+# normal build (their device code is unchanged).
+SAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+            "-Xarch_host", "-g"]
+
+
+def build_sanitized(out_dir: str) -> str:
+    """libapc.so in out_dir with apc.cpp's host code instrumented; needs a
+    normal build's objects (build() first)."""
+    os.makedirs(out_dir, exist_ok=True)
+    obj = os.path.join(out_dir, "apc_san.o")
+    cmd = [HIPCC, *FLAGS, *SAN_HOST, "-x", "hip", "-c", os.path.join(CSRC, "apc.cpp"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for the sanitized apc.cpp:\n{r.stderr}")
+    objs = [obj] + [os.path.join(BUILD, os.path.splitext(src)[0] + ".o") for src in SOURCES if src != "apc.cpp"]
+    out = os.path.join(out_dir, "libapc.so")
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-shared-libasan", *SAN_HOST, "-o", out, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stderr}")
+    return out
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

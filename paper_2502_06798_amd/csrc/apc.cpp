@@ -108,6 +108,7 @@ const char* apc_status_str(apc_status s)
     case APC_E_WORKSPACE: return "workspace too small";
     case APC_E_NOMEM: return "out of memory";
     case APC_E_HIP: return "HIP error";
+    default: break;
     }
     return "unknown status";
 }
