@@ -121,7 +121,6 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     const int64_t ngr = (n + Q8_GR - 1) / Q8_GR;                   // groups of the cache
     const int64_t g_begin = ngr * split / splits;
     const int ng = (int)(ngr * (split + 1) / splits - g_begin);   // groups of this split (>= 1)
-    const int T = ng * SPG;                                        // stages of this split
 
     // ---- queries into VGPRs (in load order), the query factor.  Wavefronts
     // past the batch compute on the zero padding of the query copy; their
@@ -158,26 +157,38 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     uint32_t voff[Q8_LPW];
 #pragma unroll
     for (int i = 0; i < Q8_LPW; ++i) voff[i] = (uint32_t)lrow(i) * RB + loff(i);
-    auto issue = [&](int s) __attribute__((always_inline)) {
-        const int se = s < T ? s : T - 1;
-        const int gi = se / SPG, j = se - gi * SPG;
-        const int64_t e0 = (g_begin + gi) * Q8_GR;
-        const uint8_t* base = emb + e0 * RB + j * Q2_SB;
-        const uint32_t m0 = lds_e + (uint32_t)(s % NS) * Q8_STAGE + (uint32_t)(wave * RPW) * Q2_SB;
-        if (e0 + Q8_GR <= n) {
+    // Stage gi SPG + D of the schedule, D a compile-time offset, for group gi
+    // whose first row is at gbase and whose first stage uses ring slot gslot
+    // (both kept up to date by the group loop, so the addresses take a few
+    // scalar additions).
+    const int64_t grp_bytes = (int64_t)Q8_GR * RB;
+    const uint8_t* const last_base = emb + (g_begin + ng - 1) * grp_bytes + (SPG - 1) * Q2_SB;   // the split's last stage
+    const int64_t tail = n - (g_begin + ng - 1) * Q8_GR;          // rows of the split's last group (<= 64)
+    auto issue = [&](int gi, const uint8_t* gbase, int gslot, auto dc) __attribute__((always_inline)) {
+        constexpr int D = decltype(dc)::value, DG = D / SPG, JJ = D % SPG;
+        const int g = gi + DG;                                     // the stage's group
+        const bool past = g >= ng;                                 // past the split: repeat its last stage
+        const uint8_t* base = past ? last_base : gbase + DG * grp_bytes + JJ * Q2_SB;
+        const int gq = past ? ng - 1 : g;
+        int slot = gslot + D;
+        if (slot >= NS) slot -= NS;
+        if (slot >= NS) slot -= NS;
+        const uint32_t m0 = lds_e + (uint32_t)slot * Q8_STAGE + (uint32_t)(wave * RPW) * Q2_SB;
+        if (gq != ng - 1 || tail == Q8_GR) {
 #pragma unroll
             for (int i = 0; i < Q8_LPW; ++i) q8_dma16(base, voff[i], m0 + i * 4 * Q2_SB);
         } else {
-            const int last = (int)(n - 1 - e0);                    // last valid row of the group
+            const int last = (int)tail - 1;                        // last valid row of the group
 #pragma unroll
             for (int i = 0; i < Q8_LPW; ++i)
                 q8_dma16(base, (uint32_t)(lrow(i) < last ? lrow(i) : last) * RB + loff(i), m0 + i * 4 * Q2_SB);
         }
         const uint32_t soff = (uint32_t)lane * 16;                 // lanes past the data idle
-        if (j == 1) {
-            if (lane < 8) q8_dma16_fresh(gthr + q0w, soff, lds_gt + (uint32_t)((gi % Q8_FR) * C::BQ + wave * 32) * 4);
+        if constexpr (JJ == 1) {
+            if (lane < 8) q8_dma16_fresh(gthr + q0w, soff, lds_gt + (uint32_t)(((gq % Q8_FR) * C::BQ + wave * 32) * 4));
         } else {
-            if (lane < Q8_GR / 4) q8_dma16(fe + e0, soff, lds_fe + (uint32_t)(gi % Q8_FR) * (Q8_GR * 4));
+            if (lane < Q8_GR / 4)
+                q8_dma16(fe + (g_begin + gq) * Q8_GR, soff, lds_fe + (uint32_t)(gq % Q8_FR) * (Q8_GR * 4));
         }
     };
     // wait until stage u has landed (this wavefront's loads; stages up to
@@ -186,8 +197,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         __builtin_amdgcn_s_waitcnt(q2_vmcnt((NS - 2) * Q8_OPS));
         __syncthreads();
     };
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s) issue(s);
+    static_for<NS - 1>([&](auto dc) __attribute__((always_inline)) { issue(0, emb + g_begin * grp_bytes, 0, dc); });
 
     // ---- list state of this lane's query.  The list's slots are split
     // between the two lanes by pairs (slots 2p, 2p + 1 belong to half p % 2);
@@ -360,21 +370,24 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     // so the successor's first fragments are read while the stage's last
     // MFMAs run (the barrier follows all reads of the stage: the slot may
     // then be refilled).  For gi = 0, prv holds zeros and nothing is tested.
-    auto group = [&](int gi, f32x16 (&acc)[Q8_EB], f32x16 (&prv)[Q8_EB]) __attribute__((always_inline)) {
+    auto group = [&](int gi, const uint8_t* gbase, int gslot, f32x16 (&acc)[Q8_EB], f32x16 (&prv)[Q8_EB])
+                     __attribute__((always_inline)) {
         const float* frp = sm.fe[(gi - 1) & (Q8_FR - 1)];
         float m = neg_inf();
         Step a0[Q8_EB], a1[Q8_EB], a2[Q8_EB];
         static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
             constexpr int j = decltype(jc)::value;
-            const int t = gi * SPG + j;
-            const uint8_t* sb = sm.e + (t % NS) * Q8_STAGE;
-            const uint8_t* sbn = sm.e + ((t + 1) % NS) * Q8_STAGE;
+            int sl = gslot + j, sln = gslot + j + 1;               // ring slots of stages t, t + 1
+            if (sl >= NS) sl -= NS;
+            if (sln >= NS) sln -= NS;
+            const uint8_t* sb = sm.e + sl * Q8_STAGE;
+            const uint8_t* sbn = sm.e + sln * Q8_STAGE;
             if constexpr (j == 0) {
                 wait_stage();
                 rd(sb, 0, a0);
                 rd(sb, 1, a1);
             }
-            issue(t + NS - 1);                                     // into the slot stage t - 1 used
+            issue(gi, gbase, gslot, std::integral_constant<int, j + NS - 1>{});   // into the slot stage t - 1 used
             static_for<SST>([&](auto sc) __attribute__((always_inline)) {
                 constexpr int ss = decltype(sc)::value;
                 constexpr int st = j * SST + ss;                   // MFMA step of the group
@@ -408,9 +421,20 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         acc0[eb] = f32x16{};
         acc1[eb] = f32x16{};
     }
+    const uint8_t* gbase = emb + g_begin * grp_bytes;
+    int gslot = 0;
+    auto next_group = [&]() __attribute__((always_inline)) {
+        gbase += grp_bytes;
+        gslot += SPG;
+        if (gslot >= NS) gslot -= NS;
+    };
     for (int gi = 0; gi < ng; gi += 2) {
-        group(gi, acc0, acc1);
-        if (gi + 1 < ng) group(gi + 1, acc1, acc0);
+        group(gi, gbase, gslot, acc0, acc1);
+        next_group();
+        if (gi + 1 < ng) {
+            group(gi + 1, gbase, gslot, acc1, acc0);
+            next_group();
+        }
     }
     __builtin_amdgcn_s_waitcnt(q2_vmcnt(0));                       // the loads past the split
     if (q0w >= b) return;
