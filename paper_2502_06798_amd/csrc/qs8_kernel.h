@@ -95,6 +95,17 @@ __device__ inline void q8_dma16_fresh(const void* base, uint32_t off, uint32_t l
     asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 sc1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
 }
 
+// the value x of the lane 32 apart (lane ^ 32), through the VALU's lane-half
+// swap rather than an LDS permute: v_permlane32_swap exchanges lanes 32..63
+// of its first operand with lanes 0..31 of its second, so with x in both,
+// the second result holds the upper half's x in lanes 0..31 and the first
+// the lower half's x in lanes 32..63.  Every lane must be active.
+__device__ inline uint32_t q8_partner(uint32_t x, int h)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return h ? (uint32_t)r[0] : (uint32_t)r[1];
+}
+
 template <int DT, int RB, int KR>
 __global__ __launch_bounds__(Q8_NT) void k_qs8(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
@@ -209,6 +220,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     int cnt = 0;                 // keys in the list
     uint64_t wkey = 0;           // its smallest key (valid once cnt == k)
     int wslot = 0;               // and that key's slot
+    float own = neg_inf();       // the list's k-th best score (-inf while cnt < k)
     uint64_t hkey = ~0ull;       // the smallest key of this lane's slots
     int hslot = 0;               // and its slot
     // the smallest of this lane's keys and its slot (four reads, eight keys,
@@ -237,11 +249,12 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     };
     // the list's smallest key and slot from both lanes' (all lanes take part)
     auto combine = [&]() __attribute__((always_inline)) {
-        const uint32_t olo = __shfl_xor((uint32_t)hkey, 32, 64), ohi = __shfl_xor((uint32_t)(hkey >> 32), 32, 64);
-        const int os = __shfl_xor(hslot, 32, 64);
+        const uint32_t olo = q8_partner((uint32_t)hkey, h), ohi = q8_partner((uint32_t)(hkey >> 32), h);
+        const int os = (int)q8_partner((uint32_t)hslot, h);
         const uint64_t ob = ((uint64_t)ohi << 32) | olo;
         wkey = ob < hkey ? ob : hkey;
         wslot = ob < hkey ? os : hslot;
+        own = cnt >= k ? q2_key_score(wkey) : neg_inf();
     };
 
     // one piece of the filter of the previous group (four of a lane's values,
@@ -269,7 +282,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     // least that much; ties with it are kept).
     auto finish = [&](int gp, int gs, f32x16 (&prv)[Q8_EB], float m) __attribute__((always_inline)) {
         const float G = q2_unkey(sm.gthr[gs & (Q8_FR - 1)][wave * 32 + r32]);
-        const float F = __builtin_fmaxf(cnt >= k ? q2_key_score(wkey) : neg_inf(), G);
+        const float F = __builtin_fmaxf(own, G);
         const bool pass = fq == fq && clamp1(m * fq) >= F;         // NaN f_q: row not matched
         if (!__builtin_amdgcn_ballot_w64(pass)) return;
         const int64_t e0 = (g_begin + gp) * Q8_GR;
@@ -319,8 +332,8 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
                 // both lanes of the query follow the inserting one (every lane
                 // takes part in the exchange: a lane whose partner is masked
                 // off would read 0)
-                const int pins = __shfl_xor((int)ins, 32, 64);
-                const bool did = h == hh ? ins : pins != 0;
+                const uint32_t pins = q8_partner((uint32_t)ins, h);
+                const bool did = h == hh ? ins : pins != 0u;
                 if (did) {
                     if (cnt < k) ++cnt;
                     if (cnt == k) rescan();
@@ -329,10 +342,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
             }
         }
         // publish this split's k-th best when it beats the shared bound
-        if (cnt >= k) {
-            const float kth = q2_key_score(wkey);
-            if (h == 0 && kth > G) q2_atomic_max(gthr + q0w + r32, q2_key(kth));
-        }
+        if (h == 0 && own > G) q2_atomic_max(gthr + q0w + r32, q2_key(own));
     };
 
     // A fragments: the per-lane byte offsets (row and swizzled unit) of the
