@@ -31,14 +31,17 @@ MALL_BYTES = 256 << 20
 
 # HBM bytes per launch of the similarity kernel from the FETCH_SIZE and
 # WRITE_SIZE counters, scaled by a plain copy's readings
-# (profiles/qs_hbm_bytes_all_workloads_pmc.md).  They hold for the kernel and
-# plan code they were taken on (hashed without comments); any other code
-# reports null.
+# (profiles/similarity_hbm_bytes_all_workloads_pmc.md).  They hold for the
+# kernel and plan code they were taken on (hashed without comments); any other
+# code reports null.
 TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_amd/csrc/qs.hip",
-                   "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "ac85d6eb1aa05c8a"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160748000, "b1024_n1m_d768_bf16": 1573725248,
-                 "b4096_n4m_d512_f16": 4369844000, "b16384_n10m_d768_e4m3": 518880819264}
+                   "paper_2502_06798_amd/csrc/qs_f16.hip", "paper_2502_06798_amd/csrc/qs_bf16.hip",
+                   "paper_2502_06798_amd/csrc/qs_e4m3.hip", "paper_2502_06798_amd/csrc/qs8_kernel.h",
+                   "paper_2502_06798_amd/csrc/qs8_f16.hip", "paper_2502_06798_amd/csrc/qs8_bf16.hip",
+                   "paper_2502_06798_amd/csrc/qs8_e4m3.hip", "paper_2502_06798_amd/csrc/simtopk.hip")
+TRAFFIC_SHA256 = "a42a158f1d6f0a37"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160773548, "b1024_n1m_d768_bf16": 1571184592,
+                 "b4096_n4m_d512_f16": 4369373394, "b16384_n10m_d768_e4m3": 129667118298}
 
 
 def log(*a):
