@@ -45,7 +45,7 @@ struct MatchPlan {
     int qtiles;        // ceil(b / bq)
     int splits;        // workgroups along the entries per query tile
     int64_t b_pad;     // qtiles * bq
-    size_t off_fq, off_gt, off_ps, off_pi, off_qp, bytes;   // workspace layout
+    size_t off_fq, off_gt, off_g2, off_ps, off_pi, off_qp, bytes;   // workspace layout
 };
 MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k);
 
@@ -73,7 +73,7 @@ int qs_group_rows(int64_t row_bytes, int k);
 // (b_pad x row_bytes bytes) receives the queries in the order that kernel's
 // lanes load them, for query tiles of bq rows over nw wavefronts
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, uint8_t* qperm, int bq, int nw, hipStream_t s);
+                        float* fq, int* gthr, uint8_t* qperm, int bq, int nw, int* g2, int nsplit, hipStream_t s);
 hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
                      hipStream_t s);
@@ -83,7 +83,8 @@ hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const voi
 int qs8_queries(int dt, int64_t row_bytes, int k);
 int qs8_group_rows();
 hipError_t launch_qs8(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
-                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                      const void* q, const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi,
+                      hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

@@ -20,7 +20,7 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, const float* __restrict__ q_scale,
                                                 int32_t b, int64_t b_pad, int64_t row_bytes,
                                                 float* __restrict__ fq, int* __restrict__ gthr,
-                                                uint8_t* __restrict__ qperm, int bq, int nw)
+                                                uint8_t* __restrict__ qperm, int bq, int nw, int* __restrict__ g2, int nsplit)
 {
     constexpr int UPS = Q2Op<DT>::UPS;
     const int lane = threadIdx.x & 63;
@@ -58,6 +58,8 @@ __global__ __launch_bounds__(256) void k_qprep(const uint8_t* __restrict__ qry, 
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
     bad = __any(bad);
+    if (g2)
+        for (int sp = lane; sp < nsplit; sp += 64) g2[(int64_t)sp * b_pad + r] = q2_key(neg_inf());
     if (lane != 0) return;
     bool ok = r < b && !bad && __builtin_isfinite(ss) && ss > 0.f;
     if (ok && q_scale) {
@@ -87,14 +89,14 @@ int qs8_queries(int dt, int64_t row_bytes, int k)
 int qs8_group_rows() { return Q8_GR; }
 
 hipError_t launch_qprep(int dt, const void* q, const float* q_scale, int32_t b, int64_t b_pad, int64_t row_bytes,
-                        float* fq, int* gthr, uint8_t* qperm, int bq, int nw, hipStream_t s)
+                        float* fq, int* gthr, uint8_t* qperm, int bq, int nw, int* g2, int nsplit, hipStream_t s)
 {
     const dim3 grid((unsigned)((b_pad + 3) / 4)), block(256);
     const uint8_t* qp = static_cast<const uint8_t*>(q);
     switch (dt) {
-    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw); break;
-    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw); break;
-    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw); break;
+    case APC_F16: k_qprep<APC_F16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw, g2, nsplit); break;
+    case APC_BF16: k_qprep<APC_BF16><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw, g2, nsplit); break;
+    case APC_E4M3: k_qprep<APC_E4M3><<<grid, block, 0, s>>>(qp, q_scale, b, b_pad, row_bytes, fq, gthr, qperm, bq, nw, g2, nsplit); break;
     default: return hipErrorInvalidValue;                          // the query-stationary kernels take 16-bit or e4m3 rows
     }
     return hipGetLastError();
@@ -114,13 +116,14 @@ hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const voi
 }
 
 hipError_t launch_qs8(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
-                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                      const void* q, const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi,
+                      hipStream_t s)
 {
     const int64_t rb = (int64_t)d * elem_bytes(dt);
     switch (dt) {
-    case APC_F16: return launch_qs8_f16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-    case APC_BF16: return launch_qs8_bf16(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-    case APC_E4M3: return launch_qs8_e4m3(p, n, rb, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+    case APC_F16: return launch_qs8_f16(p, n, rb, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
+    case APC_BF16: return launch_qs8_bf16(p, n, rb, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
+    case APC_E4M3: return launch_qs8_e4m3(p, n, rb, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
     default: return hipErrorInvalidValue;
     }
 }

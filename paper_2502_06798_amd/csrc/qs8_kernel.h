@@ -51,6 +51,8 @@ constexpr int Q8_LPW = Q8_STAGE / 1024 / Q8_NW; // row loads per wavefront per s
 constexpr int Q8_OPS = Q8_LPW + 1;              // vector-memory operations per wavefront per stage
 constexpr int Q8_FR = 8;                        // ring of per-group entry factors
 constexpr int Q8_KMAX = 32;
+constexpr int Q8_QM = 128;                      // groups between refreshes of the quantile bound
+constexpr int Q8_QSPLITS = 16;                  // most splits it is shared over
 
 template <int DT, int RB, int KR>
 struct Q8Cfg {
@@ -106,10 +108,32 @@ __device__ inline uint32_t q8_partner(uint32_t x, int h)
     return h ? (uint32_t)r[0] : (uint32_t)r[1];
 }
 
+// base[off / 4] = v and v = base[off / 4], device-coherent (sc1: written
+// through and read past this XCD's L2, so other XCDs' workgroups see them),
+// addressed as a wave-uniform base plus a per-lane offset, so that no
+// per-lane 64-bit address stays live; the load waits for every vector-memory
+// operation in flight (the ring's loads too: they are counted by hand, out of
+// the compiler's view)
+__device__ inline void q8_store(const int* base, uint32_t off, int v)
+{
+    asm volatile("global_store_dword %0, %1, %2 sc1" ::"v"(off), "v"(v), "s"(base) : "memory");
+}
+__device__ inline int q8_load_now(const int* base, uint32_t off)
+{
+    int v;
+    asm volatile("global_load_dword %0, %1, %2 sc1\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(off), "s"(base) : "memory");
+    return v;
+}
+// device-scope signed max of v into base[off / 4]
+__device__ inline void q8_atomic_max(const int* base, uint32_t off, int v)
+{
+    asm volatile("global_atomic_smax %0, %1, %2" ::"v"(off), "v"(v), "s"(base) : "memory");
+}
+
 template <int DT, int RB, int KR>
 __global__ __launch_bounds__(Q8_NT) void k_qs8(
     const uint8_t* __restrict__ emb, const float* __restrict__ fe, int64_t n,
-    const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int32_t b,
+    const uint8_t* __restrict__ qry, const float* __restrict__ fq_ws, int* __restrict__ gthr, int* __restrict__ g2, int32_t b,
     int32_t k, int splits, int qtiles, float* __restrict__ part_s, int* __restrict__ part_i)
 {
     typedef Q8Cfg<DT, RB, KR> C;
@@ -165,9 +189,10 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     // logical unit (lane % 16) ^ (row % 16) of it stored at unit lane % 16
     auto lrow = [&](int i) __attribute__((always_inline)) { return wave * RPW + i * 4 + (lane >> 4); };
     auto loff = [&](int i) __attribute__((always_inline)) { return (uint32_t)(((lane & 15) ^ (lrow(i) & 15)) * 16); };
-    uint32_t voff[Q8_LPW];
-#pragma unroll
-    for (int i = 0; i < Q8_LPW; ++i) voff[i] = (uint32_t)lrow(i) * RB + loff(i);
+    // (load 1's row is load 0's + 4, whose low four bits differ in bit 2
+    // only: its unit offset is load 0's ^ 64, and RB is a multiple of 256)
+    static_assert(Q8_LPW == 2, "two row loads per wavefront and stage");
+    const uint32_t voff0 = (uint32_t)lrow(0) * RB + loff(0);
     // Stage gi SPG + D of the schedule, D a compile-time offset, for group gi
     // whose first row is at gbase and whose first stage uses ring slot gslot
     // (both kept up to date by the group loop, so the addresses take a few
@@ -187,7 +212,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         const uint32_t m0 = lds_e + (uint32_t)slot * Q8_STAGE + (uint32_t)(wave * RPW) * Q2_SB;
         if (gq != ng - 1 || tail == Q8_GR) {
 #pragma unroll
-            for (int i = 0; i < Q8_LPW; ++i) q8_dma16(base, voff[i], m0 + i * 4 * Q2_SB);
+            for (int i = 0; i < Q8_LPW; ++i) q8_dma16(base, i ? (voff0 ^ 64u) + 4 * RB : voff0, m0 + i * 4 * Q2_SB);
         } else {
             const int last = (int)tail - 1;                        // last valid row of the group
 #pragma unroll
@@ -342,31 +367,90 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
             }
         }
         // publish this split's k-th best when it beats the shared bound
-        if (h == 0 && own > G) q2_atomic_max(gthr + q0w + r32, q2_key(own));
+        if (h == 0 && own > G) q8_atomic_max(gthr + q0w, (uint32_t)r32 * 4, q2_key(own));
     };
 
-    // A fragments: the per-lane byte offsets (row and swizzled unit) of the
-    // first unit each step of a stage reads, fixed for the kernel; block eb
+    // A second bound, shared through the same slot.  Split s publishes, per
+    // query, a score v_s that at least r = ceil(k / splits) keys of its list
+    // reach: the smaller of its two halves' ceil(r / 2)-th largest (the
+    // larger of the two maxima when r = 1).  The splits' rows are disjoint,
+    // so at least splits * r >= k keys reach min_s v_s: a lower bound on the
+    // query's k-th best, whatever each split's progress (a list only
+    // improves, so an old v_s stays valid).  For splits of equal progress it
+    // is about the k-th best of all their rows together, where each split's
+    // own k-th is that of a quarter of them (with four splits).  It is
+    // refreshed every Q8_QM groups: a scan of the list, one store, and one
+    // load per split.
+    const int64_t b_pad = (int64_t)qtiles * C::BQ;
+    auto share_quantile = [&]() __attribute__((always_inline)) {
+        const int rq = (k + splits - 1) / splits, rh = (rq + 1) / 2;
+        // this lane's slots' rh-th largest order word (the key's upper 32
+        // bits; counting equal words; 0 if the half holds fewer), by rh
+        // passes over the slots, each finding the largest word below the
+        // previous pass's and how often it occurs
+        constexpr int HS = KR / 2;
+        const uint32_t* const lw = reinterpret_cast<const uint32_t*>(lst);   // word 2 c + 1: slot c's order word
+        uint32_t prev = ~0u, u = 0u;
+        int need = rh;
+        bool found = false;
+#pragma unroll 1
+        for (int it = 0; it < rh; ++it) {
+            asm volatile("" ::: "memory");                         // read the slots again: no copy held in registers
+            uint32_t mx = 0u;
+            int c = 0;
+#pragma unroll 2
+            for (int i = 0; i < HS; ++i) {
+                const int sl = 2 * h + 4 * (i >> 1) + (i & 1);     // this half's slots
+                uint32_t x = sl < cnt ? lw[2 * sl + 1] : 0u;
+                x = x < prev ? x : 0u;
+                c = x > mx ? 1 : c + (x == mx ? 1 : 0);
+                mx = x > mx ? x : mx;
+            }
+            if (!found && mx != 0u) {
+                if (c >= need) {
+                    u = mx;
+                    found = true;
+                } else {
+                    need -= c;
+                    prev = mx;
+                }
+            }
+        }
+        const uint32_t uo = q8_partner(u, h);
+        const uint32_t v = rq <= 1 ? __builtin_elementwise_max(u, uo) : __builtin_elementwise_min(u, uo);
+        const int key = q2_key(q2_key_score((uint64_t)v << 32));  // -inf for 0
+        if (h == 0) {
+            const uint32_t off = (uint32_t)r32 * 4;
+            q8_store(g2 + split * b_pad + q0w, off, key);
+            int mn = key;
+            for (int sp = 0; sp < splits; ++sp) mn = __builtin_elementwise_min(mn, q8_load_now(g2 + sp * b_pad + q0w, off));
+            if (mn > q2_key(neg_inf())) q8_atomic_max(gthr + q0w, off, mn);
+        }
+    };
+
+    // A fragments: the per-lane byte offset (row and swizzled unit) of the
+    // first unit a step of a stage reads, fixed for the kernel; block eb
     // adds eb 8 KB.  An e4m3 step's second unit is logical unit lu + 1 (lu
     // even), stored at unit (lu ^ x) ^ 1: its offset is the first's ^ 16
     // (stage and row offsets are multiples of 256).
-    uint32_t uo[SST];
-#pragma unroll
-    for (int ss = 0; ss < SST; ++ss) {
+    // Step ss reads logical unit lu = 4 h + c (c = 8 cl + sp has no bit in
+    // common with 4 h), stored at unit lu ^ (r32 % 16) = (4 h ^ (r32 % 16)) ^ c:
+    // one offset per lane, uo0, and a constant per step.
+    const uint32_t uo0 = (uint32_t)(r32 * Q2_SB + (((h * 4) ^ (r32 & 15)) * 16));
+    auto uo = [&](int ss) __attribute__((always_inline)) {
         const int cl = ss / (4 / UPS), sp = (ss % (4 / UPS)) * UPS;
-        const int lu = cl * 8 + h * 4 + sp;                        // logical 16-byte unit
-        uo[ss] = (uint32_t)(r32 * Q2_SB + ((lu ^ (r32 & 15)) * 16));
-    }
+        return uo0 ^ (uint32_t)((cl * 8 + sp) * 16);
+    };
     auto rd = [&](const uint8_t* sbase, int ss, Step (&dst)[Q8_EB]) __attribute__((always_inline)) {
         const uint32_t base = (uint32_t)(size_t)(lds_void*)sbase;
-        const uint32_t a0 = base + uo[ss];
+        const uint32_t a0 = base + uo(ss);
 #pragma unroll
         for (int eb = 0; eb < Q8_EB; ++eb) {
             const uint8_t* rp = sbase + eb * 32 * Q2_SB;
             if constexpr (UPS == 1) {
-                dst[eb] = *reinterpret_cast<const uint4*>(rp + uo[ss]);
+                dst[eb] = *reinterpret_cast<const uint4*>(rp + uo(ss));
             } else {
-                const uint4 x0 = *reinterpret_cast<const uint4*>(rp + uo[ss]);
+                const uint4 x0 = *reinterpret_cast<const uint4*>(rp + uo(ss));
                 const uint4 x1 = *reinterpret_cast<const uint4*>(rp + ((a0 ^ 16u) - base));
                 dst[eb] = Step{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w, (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
             }
@@ -423,6 +507,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
             });
         });
         if (gi >= 1) finish(gi - 1, gi, prv, m);
+        if ((gi & (Q8_QM - 1)) == Q8_QM - 1 && splits > 1 && splits <= Q8_QSPLITS) share_quantile();
     };
 
     f32x16 acc0[Q8_EB], acc1[Q8_EB];
@@ -496,12 +581,12 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
 
 template <int DT, int RB, int KR>
 hipError_t run_qs8(const MatchPlan& p, int64_t n, const void* emb, const float* fe, const void* q, const float* fq,
-                   int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                   int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
     const int work = p.splits * p.qtiles;
     const int grid = work >= 8 ? (work + 7) / 8 * 8 : work;
     k_qs8<DT, RB, KR><<<grid, Q8_NT, 0, s>>>(static_cast<const uint8_t*>(emb), fe, n, static_cast<const uint8_t*>(q),
-                                              fq, gthr, b, k, p.splits, p.qtiles, ps, pi);
+                                              fq, gthr, g2, b, k, p.splits, p.qtiles, ps, pi);
     return hipGetLastError();
 }
 
@@ -511,23 +596,23 @@ constexpr bool q8_built(int64_t row_bytes, int k) { return (row_bytes == 512 || 
 
 template <int DT>
 hipError_t q8_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                       const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
+                       const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
     if (k <= 16) {
-        if (rb == 768) return run_qs8<DT, 768, 16>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-        if (rb == 512) return run_qs8<DT, 512, 16>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+        if (rb == 768) return run_qs8<DT, 768, 16>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
+        if (rb == 512) return run_qs8<DT, 512, 16>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
     } else if (k <= Q8_KMAX) {
-        if (rb == 768) return run_qs8<DT, 768, 32>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s);
-        if (rb == 512) return run_qs8<DT, 512, 32>(p, n, emb, fe, q, fq, gthr, b, k, ps, pi, s);
+        if (rb == 768) return run_qs8<DT, 768, 32>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
+        if (rb == 512) return run_qs8<DT, 512, 32>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
     }
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_qs8_f16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                          const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                          const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 hipError_t launch_qs8_bf16(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                           const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                           const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 hipError_t launch_qs8_e4m3(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
-                           const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
+                           const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 
 }  // namespace apc

@@ -539,7 +539,10 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
     p.b_pad = (int64_t)p.qtiles * p.bq;
     p.off_fq = 0;
     p.off_gt = align256(p.off_fq + sizeof(float) * (size_t)p.b_pad);
-    p.off_ps = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
+    // the two-wavefront kernel's per-split quantile scores (splits x b_pad)
+    p.off_g2 = align256(p.off_gt + sizeof(int) * (size_t)p.b_pad);
+    const size_t g2_bytes = p.kernel == KERNEL_QS8 ? sizeof(int) * (size_t)p.splits * p.b_pad : 0;
+    p.off_ps = align256(p.off_g2 + g2_bytes);
     p.off_pi = align256(p.off_ps + sizeof(float) * (size_t)p.splits * p.b_pad * k);
     p.off_qp = align256(p.off_pi + sizeof(int) * (size_t)p.splits * p.b_pad * k);
     const size_t qp_bytes =
@@ -572,15 +575,18 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
         uint8_t* qp = w + p.off_qp;
-        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 4, s)) != hipSuccess) return e;
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 4, nullptr, 0, s)) != hipSuccess)
+            return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_qs(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QS8) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
         uint8_t* qp = w + p.off_qp;
-        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 8, s)) != hipSuccess) return e;
+        int* g2 = reinterpret_cast<int*>(w + p.off_g2);
+        if ((e = launch_qprep(dt, q, q_scale, b, p.b_pad, row_bytes, fq, gt, qp, p.bq, 8, g2, p.splits, s)) != hipSuccess)
+            return e;
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
-        e = launch_qs8(p, dt, n, d, emb, fe, qp, fq, gt, b, k, ps, pi, s);
+        e = launch_qs8(p, dt, n, d, emb, fe, qp, fq, gt, g2, b, k, ps, pi, s);
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
         e = launch_stream(p, dt, n, d, emb, fe, q, q_scale, b, k, fq, ps, pi, s);
