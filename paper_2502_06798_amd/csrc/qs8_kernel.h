@@ -70,6 +70,7 @@ struct Q8Cfg {
     static_assert(RB == 512 || RB == 768, "rows of two or three stages");
     static_assert(NSTEP >= 8, "the filter of a group is spread over eight MFMA steps");
     static_assert(SST >= 3, "fragments are read two steps ahead, within the stage for its first steps");
+    static_assert(Q8_OPS <= SST - 1, "a stage's loads are issued by the step of its wait for the next stage");
     static_assert(NS >= 4, "LDS ring too small");
     // The entry factors of group g (slot g % FR) are read until the end of
     // group g + 1; the loads of group g + FR start NS - 1 stages early.
@@ -194,37 +195,62 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     static_assert(Q8_LPW == 2, "two row loads per wavefront and stage");
     const uint32_t voff0 = (uint32_t)lrow(0) * RB + loff(0);
     // Stage gi SPG + D of the schedule, D a compile-time offset, for group gi
-    // whose first row is at gbase and whose first stage uses ring slot gslot
-    // (both kept up to date by the group loop, so the addresses take a few
-    // scalar additions).
+    // whose first row is at gbase, whose entry factors are at fbase and whose
+    // first stage uses ring slot gslot (all kept up to date by the group loop,
+    // so the addresses of a group inside the split take a few scalar
+    // additions; only the split's last group and the stages past it take the
+    // general path).
     const int64_t grp_bytes = (int64_t)Q8_GR * RB;
     const uint8_t* const last_base = emb + (g_begin + ng - 1) * grp_bytes + (SPG - 1) * Q2_SB;   // the split's last stage
     const int64_t tail = n - (g_begin + ng - 1) * Q8_GR;          // rows of the split's last group (<= 64)
-    auto issue = [&](int gi, const uint8_t* gbase, int gslot, auto dc) __attribute__((always_inline)) {
-        constexpr int D = decltype(dc)::value, DG = D / SPG, JJ = D % SPG;
+    // Part P < Q8_LPW is row load P, part Q8_LPW the side load; a part
+    // outside [0, Q8_OPS) issues all of them.
+    auto issue = [&](int gi, const uint8_t* gbase, const float* fbase, int gslot, auto dc, auto pc)
+                     __attribute__((always_inline)) {
+        constexpr int D = decltype(dc)::value, DG = D / SPG, JJ = D % SPG, P = decltype(pc)::value;
+        constexpr bool all = P < 0 || P >= Q8_OPS;
+        auto row_part = [&](int i) __attribute__((always_inline)) { return all || P == i; };
+        constexpr bool side_part = all || P == Q8_LPW;
         const int g = gi + DG;                                     // the stage's group
-        const bool past = g >= ng;                                 // past the split: repeat its last stage
-        const uint8_t* base = past ? last_base : gbase + DG * grp_bytes + JJ * Q2_SB;
-        const int gq = past ? ng - 1 : g;
         int slot = gslot + D;
         if (slot >= NS) slot -= NS;
         if (slot >= NS) slot -= NS;
         const uint32_t m0 = lds_e + (uint32_t)slot * Q8_STAGE + (uint32_t)(wave * RPW) * Q2_SB;
-        if (gq != ng - 1 || tail == Q8_GR) {
-#pragma unroll
-            for (int i = 0; i < Q8_LPW; ++i) q8_dma16(base, i ? (voff0 ^ 64u) + 4 * RB : voff0, m0 + i * 4 * Q2_SB);
-        } else {
-            const int last = (int)tail - 1;                        // last valid row of the group
+        const uint32_t soff = (uint32_t)lane * 16;                 // lanes past the side data idle
+        // the side load of group gq into its ring slot
+        auto side = [&](int gq, const float* fg) __attribute__((always_inline)) {
+            if constexpr (!side_part) return;
+            if constexpr (JJ == 1) {
+                if (lane < 8)
+                    q8_dma16_fresh(gthr + q0w, soff, lds_gt + (uint32_t)(((gq & (Q8_FR - 1)) * C::BQ + wave * 32) * 4));
+            } else {
+                if (lane < Q8_GR / 4) q8_dma16(fg, soff, lds_fe + (uint32_t)(gq & (Q8_FR - 1)) * (Q8_GR * 4));
+            }
+        };
+        if (g < ng - 1) {
+            // a whole group inside the split: constant offsets from the running bases
+            const uint8_t* base = gbase + DG * grp_bytes + JJ * Q2_SB;
 #pragma unroll
             for (int i = 0; i < Q8_LPW; ++i)
-                q8_dma16(base, (uint32_t)(lrow(i) < last ? lrow(i) : last) * RB + loff(i), m0 + i * 4 * Q2_SB);
-        }
-        const uint32_t soff = (uint32_t)lane * 16;                 // lanes past the data idle
-        if constexpr (JJ == 1) {
-            if (lane < 8) q8_dma16_fresh(gthr + q0w, soff, lds_gt + (uint32_t)(((gq % Q8_FR) * C::BQ + wave * 32) * 4));
+                if (row_part(i)) q8_dma16(base, i ? (voff0 ^ 64u) + 4 * RB : voff0, m0 + i * 4 * Q2_SB);
+            side(g, fbase + DG * Q8_GR);
         } else {
-            if (lane < Q8_GR / 4)
-                q8_dma16(fe + (g_begin + gq) * Q8_GR, soff, lds_fe + (uint32_t)(gq % Q8_FR) * (Q8_GR * 4));
+            // the split's last group (its rows past the cache repeat its last
+            // row), or past the split (a repeat of its last stage)
+            const bool past = g >= ng;
+            const uint8_t* base = past ? last_base : gbase + DG * grp_bytes + JJ * Q2_SB;
+            if (tail == Q8_GR) {
+#pragma unroll
+                for (int i = 0; i < Q8_LPW; ++i)
+                    if (row_part(i)) q8_dma16(base, i ? (voff0 ^ 64u) + 4 * RB : voff0, m0 + i * 4 * Q2_SB);
+            } else {
+                const int last = (int)tail - 1;                    // last valid row of the group
+#pragma unroll
+                for (int i = 0; i < Q8_LPW; ++i)
+                    if (row_part(i))
+                        q8_dma16(base, (uint32_t)(lrow(i) < last ? lrow(i) : last) * RB + loff(i), m0 + i * 4 * Q2_SB);
+            }
+            side(ng - 1, fe + (g_begin + ng - 1) * Q8_GR);
         }
     };
     // wait until stage u has landed (this wavefront's loads; stages up to
@@ -233,7 +259,9 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         __builtin_amdgcn_s_waitcnt(q2_vmcnt((NS - 2) * Q8_OPS));
         __syncthreads();
     };
-    static_for<NS - 1>([&](auto dc) __attribute__((always_inline)) { issue(0, emb + g_begin * grp_bytes, 0, dc); });
+    static_for<NS - 1>([&](auto dc) __attribute__((always_inline)) {
+        issue(0, emb + g_begin * grp_bytes, fe + g_begin * Q8_GR, 0, dc, std::integral_constant<int, -1>{});
+    });
 
     // ---- list state of this lane's query.  The list's slots are split
     // between the two lanes by pairs (slots 2p, 2p + 1 belong to half p % 2);
@@ -464,7 +492,8 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     // so the successor's first fragments are read while the stage's last
     // MFMAs run (the barrier follows all reads of the stage: the slot may
     // then be refilled).  For gi = 0, prv holds zeros and nothing is tested.
-    auto group = [&](int gi, const uint8_t* gbase, int gslot, f32x16 (&acc)[Q8_EB], f32x16 (&prv)[Q8_EB])
+    auto group = [&](int gi, const uint8_t* gbase, const float* fbase, int gslot, f32x16 (&acc)[Q8_EB],
+                     f32x16 (&prv)[Q8_EB])
                      __attribute__((always_inline)) {
         const float* frp = sm.fe[(gi - 1) & (Q8_FR - 1)];
         float m = neg_inf();
@@ -481,11 +510,16 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
                 rd(sb, 0, a0);
                 rd(sb, 1, a1);
             }
-            issue(gi, gbase, gslot, std::integral_constant<int, j + NS - 1>{});   // into the slot stage t - 1 used
             static_for<SST>([&](auto sc) __attribute__((always_inline)) {
                 constexpr int ss = decltype(sc)::value;
                 constexpr int st = j * SST + ss;                   // MFMA step of the group
                 constexpr int tg = ss + 2;                         // step whose fragments are read now
+                // the stage's loads into the slot stage t - 1 used, one per
+                // step (all before the wait at step SST - 2, whose count
+                // includes them), so that the workgroup's loads are not one
+                // burst after the barrier
+                if constexpr (ss < Q8_OPS)
+                    issue(gi, gbase, fbase, gslot, std::integral_constant<int, j + NS - 1>{}, std::integral_constant<int, ss>{});
                 if constexpr (tg < SST) {
                     rd(sb, tg, a2);
                 } else if constexpr (j + 1 < SPG) {
@@ -517,17 +551,19 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         acc1[eb] = f32x16{};
     }
     const uint8_t* gbase = emb + g_begin * grp_bytes;
+    const float* fbase = fe + g_begin * Q8_GR;
     int gslot = 0;
     auto next_group = [&]() __attribute__((always_inline)) {
         gbase += grp_bytes;
+        fbase += Q8_GR;
         gslot += SPG;
         if (gslot >= NS) gslot -= NS;
     };
     for (int gi = 0; gi < ng; gi += 2) {
-        group(gi, gbase, gslot, acc0, acc1);
+        group(gi, gbase, fbase, gslot, acc0, acc1);
         next_group();
         if (gi + 1 < ng) {
-            group(gi + 1, gbase, gslot, acc1, acc0);
+            group(gi + 1, gbase, fbase, gslot, acc1, acc0);
             next_group();
         }
     }
