@@ -360,10 +360,21 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     // stage j of the group adds j * 256 to them (not through the load's offset
     // field: for loads into LDS that offset moves the LDS address too)
     const uint8_t* rowp[LPW];
-    auto issue = [&](int gi, auto jc) __attribute__((always_inline)) {                            // stage j of group gi
+    // Part p of NP (SST - LA + 1 or 1) issues the bounds (p = 0),
+    // the row loads i with i % NP == p, then the entry factors (p = NP - 1),
+    // in that order; a negative part issues everything.  The stage loop issues part p at its
+    // step p, all before its wait for the next stage, so the order of the
+    // loads, and with it every wait count, is that of issuing them at once.
+    constexpr int LA = SST < 3 ? SST : 2;
+    // (spread only for 16-bit rows with one query block per wavefront: e4m3
+    // rows run out of registers, and with two blocks, four MFMAs per step,
+    // spreading was slower)
+    constexpr int NP = UPS == 1 && MQ == 1 ? SST - LA + 1 : 1;
+    auto issue = [&](int gi, auto jc, int part) __attribute__((always_inline)) {                  // stage j of group gi
         constexpr int j = decltype(jc)::value;
+        const bool all = part < 0;
         if constexpr (j == 0) {
-            if (gi >= 1) {
+            if (gi >= 1 && (all || part == 0)) {
                 // the previous group's global bounds, for its epilogue: this
                 // wavefront's queries, one load, lanes beyond the data idle
                 const int gl = lane < BQW / 4 ? lane : 0;
@@ -375,34 +386,38 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
         }
         const int64_t e0 = (g_begin + gi) * GR;
         if constexpr (j == 0) {
-            const int64_t last = n - 1 - e0;                       // last valid row of the group
+            if (all || part == 0) {
+                const int64_t last = n - 1 - e0;                   // last valid row of the group
 #pragma unroll
-            for (int i = 0; i < LPW; ++i) {
-                const int64_t row = lrow[i] < last ? lrow[i] : last;
-                rowp[i] = emb + (e0 + row) * RB + loff[i];
+                for (int i = 0; i < LPW; ++i) {
+                    const int64_t row = lrow[i] < last ? lrow[i] : last;
+                    rowp[i] = emb + (e0 + row) * RB + loff[i];
+                }
             }
         }
         const int t = gi * SPG + j;
         const uint32_t sbase = lds_e + (uint32_t)(t % NS) * STAGE;
 #pragma unroll
         for (int i = 0; i < LPW; ++i)
-            q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
-                                              sbase + (uint32_t)(wave * (GR / Q2_NW) + i * 4) * Q2_SB));
+            if (all || i % NP == part)
+                q2_dma16(rowp[i] + j * Q2_SB, __builtin_amdgcn_readfirstlane(
+                                                  sbase + (uint32_t)(wave * (GR / Q2_NW) + i * 4) * Q2_SB));
         if constexpr (j == 0) {
             // the group's GR entry factors (zero-padded to whole groups): one load,
             // lanes beyond the data idle
             const int fl = lane < GR / 4 ? lane : 0;
-            if (lane < GR / 4) q2_dma16(fe + e0 + fl * 4, lds_fe + (uint32_t)(gi % Q2_FR) * (GR * 4));
+            if ((all || part == NP - 1) && lane < GR / 4)
+                q2_dma16(fe + e0 + fl * 4, lds_fe + (uint32_t)(gi % Q2_FR) * (GR * 4));
         }
     };
     // stage s = t0 + d of the schedule, with t0 = gi0 * SPG + j0 (j0, d compile-time)
-    auto issue_ahead = [&](int gi0, auto j0c, auto dc) __attribute__((always_inline)) {
+    auto issue_ahead = [&](int gi0, auto j0c, auto dc, int part) __attribute__((always_inline)) {
         constexpr int js = (decltype(j0c)::value + decltype(dc)::value) % SPG;
         constexpr int dg = (decltype(j0c)::value + decltype(dc)::value) / SPG;
-        issue(gi0 + dg, std::integral_constant<int, js>{});
+        issue(gi0 + dg, std::integral_constant<int, js>{}, part);
     };
     static_for<NS - 1>([&](auto sc) __attribute__((always_inline)) {
-        if (decltype(sc)::value <= T) issue_ahead(0, std::integral_constant<int, 0>{}, sc);
+        if (decltype(sc)::value <= T) issue_ahead(0, std::integral_constant<int, 0>{}, sc, -1);
     });
 
     // ---- queries into VGPRs, factors, empty lists ----
@@ -467,7 +482,6 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
     // between the two points, so the wait counts are those of the next stage;
     // the barrier comes after all of this stage's reads (it waits for them),
     // so the next stage may refill this stage's slot.
-    constexpr int LA = SST < 3 ? SST : 2;
     auto run_group = [&](int gi) __attribute__((always_inline)) {
         Step an[LA][EB];                                           // the next stage's first fragments
         static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
@@ -518,8 +532,9 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
                     }
                 }
             }
-            if (t + NS - 1 <= T)                                   // into the slot stage t - 1 used
-                issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{});
+            const bool issue_now = t + NS - 1 <= T;                // into the slot stage t - 1 used
+            if (issue_now && (NP == 1 || !live))
+                issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{}, -1);
             if (!live) {
                 wait_next();
                 return;
@@ -527,6 +542,8 @@ __global__ __launch_bounds__(Q2_NT) void k_qs(
 
 #pragma unroll
             for (int ss = 0; ss < SST; ++ss) {
+                if (NP > 1 && ss < NP && issue_now)
+                    issue_ahead(gi, std::integral_constant<int, j>{}, std::integral_constant<int, NS - 1>{}, ss);
                 if (ss + LA < SST) rd(sb, ss + LA, a[ss + LA]);
                 if constexpr (ahead) {
                     if (ss == SST - LA) wait_next();
