@@ -78,7 +78,7 @@ hipError_t launch_qs(const MatchPlan& p, int dt, int64_t n, int32_t d, const voi
                      const void* q, const float* fq, int* gthr, int32_t b, int32_t k, float* ps, int* pi,
                      hipStream_t s);
 // the same with two wavefronts per SIMD and the top-k lists in LDS, for
-// 16-bit and e4m3 rows of 512 or 768 bytes (k <= 32): qs8_queries gives the
+// 16-bit and e4m3 rows of 512, 768 or 1024 bytes (k <= 32): qs8_queries gives the
 // queries per workgroup (0: not built), qs8_group_rows the rows per group
 int qs8_queries(int dt, int64_t row_bytes, int k);
 int qs8_group_rows();

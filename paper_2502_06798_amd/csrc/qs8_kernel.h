@@ -1,5 +1,5 @@
 // Query-stationary similarity + exact top-k with two wavefronts per SIMD,
-// for 16-bit and e4m3 rows of 512 or 768 bytes (k <= 32), large batches.
+// for 16-bit and e4m3 rows of 512, 768 or 1024 bytes (k <= 32), large batches.
 //
 // Grid: splits x query tiles of 256 queries.  A workgroup of eight
 // wavefronts (two per SIMD) owns a query tile and a contiguous range of cache
@@ -19,8 +19,8 @@
 // instruction stream mixes the two, and the SIMD interleaves two such
 // streams, so the matrix unit keeps busy through the other wavefront's
 // filter work and LDS waits.  The price is a register budget of 256 per
-// lane: queries (up to 96), two accumulator sets (64), the A fragments of
-// two steps; the top-k lists therefore live in LDS.
+// lane: queries (up to 128), two accumulator sets (64), the A fragments of
+// two steps (one for 1024-byte rows); the top-k lists therefore live in LDS.
 //
 // Top-k, per query: one list of k (score, entry) keys in LDS, shared by the
 // query's two lanes (they see disjoint rows of each block), unsorted, with
@@ -62,15 +62,18 @@ struct Q8Cfg {
     static constexpr int SST = Q2_SB / 32 / UPS;      // MFMA steps per stage
     static constexpr int QST = RB / 32 / UPS;         // steps of a query row held by a lane
     static constexpr int NSTEP = SPG * SST;           // MFMA steps per group
+    // steps between an A fragment's read and its MFMA: one for 1024-byte rows,
+    // whose 128 VGPRs of queries leave no room for a third fragment set
+    static constexpr int LA = RB > 768 ? 1 : 2;
     static constexpr int BQ = Q8_NW * 32;             // queries per workgroup
     static constexpr int LSTR = KR * 8 + 16;          // bytes per query list (padded: no bank conflicts)
     static constexpr int LIST_BYTES = BQ * LSTR;
     static constexpr int SIDE_BYTES = Q8_FR * Q8_GR * 4 + Q8_FR * BQ * 4;
     static constexpr int NS = (Q2_LDS - LIST_BYTES - SIDE_BYTES) / Q8_STAGE;   // stages in the ring
-    static_assert(RB == 512 || RB == 768, "rows of two or three stages");
+    static_assert(RB == 512 || RB == 768 || RB == 1024, "rows of two to four stages");
     static_assert(NSTEP >= 8, "the filter of a group is spread over eight MFMA steps");
-    static_assert(SST >= 3, "fragments are read two steps ahead, within the stage for its first steps");
-    static_assert(Q8_OPS <= SST - 1, "a stage's loads are issued by the step of its wait for the next stage");
+    static_assert(SST >= 3, "fragments are read up to two steps ahead, within the stage for its first steps");
+    static_assert(Q8_OPS <= SST - LA + 1, "a stage's loads are issued by the step of its wait for the next stage");
     static_assert(NS >= 4, "LDS ring too small");
     // The entry factors of group g (slot g % FR) are read until the end of
     // group g + 1; the loads of group g + FR start NS - 1 stages early.
@@ -487,8 +490,8 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
 
     // group gi: its MFMAs into acc; the filter of group gi - 1 (in prv) spread
     // over them; then the exact test and insertions of group gi - 1.  The A
-    // fragments are read two steps ahead of their MFMAs.  The wait and
-    // barrier for a stage's successor come two steps before the stage's end,
+    // fragments are read LA steps ahead of their MFMAs.  The wait and
+    // barrier for a stage's successor come LA steps before the stage's end,
     // so the successor's first fragments are read while the stage's last
     // MFMAs run (the barrier follows all reads of the stage: the slot may
     // then be refilled).  For gi = 0, prv holds zeros and nothing is tested.
@@ -508,12 +511,13 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
             if constexpr (j == 0) {
                 wait_stage();
                 rd(sb, 0, a0);
-                rd(sb, 1, a1);
+                if constexpr (C::LA == 2) rd(sb, 1, a1);
             }
             static_for<SST>([&](auto sc) __attribute__((always_inline)) {
                 constexpr int ss = decltype(sc)::value;
                 constexpr int st = j * SST + ss;                   // MFMA step of the group
-                constexpr int tg = ss + 2;                         // step whose fragments are read now
+                constexpr int tg = ss + C::LA;                     // step whose fragments are read now
+                Step (&an)[Q8_EB] = C::LA == 2 ? a2 : a1;          // where they go
                 // the stage's loads into the slot stage t - 1 used, one per
                 // step (all before the wait at step SST - 2, whose count
                 // includes them), so that the workgroup's loads are not one
@@ -521,10 +525,10 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
                 if constexpr (ss < Q8_OPS)
                     issue(gi, gbase, fbase, gslot, std::integral_constant<int, j + NS - 1>{}, std::integral_constant<int, ss>{});
                 if constexpr (tg < SST) {
-                    rd(sb, tg, a2);
+                    rd(sb, tg, an);
                 } else if constexpr (j + 1 < SPG) {
                     if constexpr (tg == SST) wait_stage();
-                    rd(sbn, tg - SST, a2);
+                    rd(sbn, tg - SST, an);
                 }
 #pragma unroll
                 for (int eb = 0; eb < Q8_EB; ++eb) q2_mma<DT>(acc[eb], a0[eb], qv[st], st == 0);
@@ -535,7 +539,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
 #pragma unroll
                 for (int eb = 0; eb < Q8_EB; ++eb) {
                     a0[eb] = a1[eb];
-                    a1[eb] = a2[eb];
+                    if constexpr (C::LA == 2) a1[eb] = a2[eb];
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
@@ -628,16 +632,21 @@ hipError_t run_qs8(const MatchPlan& p, int64_t n, const void* emb, const float* 
 
 }  // namespace
 
-constexpr bool q8_built(int64_t row_bytes, int k) { return (row_bytes == 512 || row_bytes == 768) && k >= 1 && k <= Q8_KMAX; }
+constexpr bool q8_built(int64_t row_bytes, int k)
+{
+    return (row_bytes == 512 || row_bytes == 768 || row_bytes == 1024) && k >= 1 && k <= Q8_KMAX;
+}
 
 template <int DT>
 hipError_t q8_dispatch(const MatchPlan& p, int64_t n, int64_t rb, const void* emb, const float* fe, const void* q,
                        const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s)
 {
     if (k <= 16) {
+        if (rb == 1024) return run_qs8<DT, 1024, 16>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
         if (rb == 768) return run_qs8<DT, 768, 16>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
         if (rb == 512) return run_qs8<DT, 512, 16>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
     } else if (k <= Q8_KMAX) {
+        if (rb == 1024) return run_qs8<DT, 1024, 32>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
         if (rb == 768) return run_qs8<DT, 768, 32>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
         if (rb == 512) return run_qs8<DT, 512, 32>(p, n, emb, fe, q, fq, gthr, g2, b, k, ps, pi, s);
     }

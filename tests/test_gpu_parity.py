@@ -181,7 +181,7 @@ def test_match_many_groups_per_split(apc, orc, dtype, b, n, d, k):
     c.close()
 
 
-# Batches above 256 queries with 512- or 768-byte rows go to the kernel with
+# Batches above 256 queries with 512-, 768- or 1024-byte rows go to the kernel with
 # two wavefronts per SIMD (256 queries per workgroup, lists in LDS): every row
 # type, both list sizes (k <= 16 and k <= 32), k = 1 and k = 32, a last group
 # of fewer than 64 rows, a cache smaller than one group, wavefronts without
@@ -195,6 +195,9 @@ QS8_CASES = [
     ("f16", 2080, 30001, 256, 32),
     ("bf16", 1024, 7000, 384, 5),
     ("e4m3", 4099, 40000, 768, 32),
+    ("f16", 1030, 20001, 512, 16),     # 1024-byte rows: fragments read one step ahead
+    ("bf16", 600, 9000, 512, 32),
+    ("e4m3", 777, 15000, 1024, 20),
 ]
 
 
