@@ -215,8 +215,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         auto row_part = [&](int i) __attribute__((always_inline)) { return all || P == i; };
         constexpr bool side_part = all || P == Q8_LPW;
         const int g = gi + DG;                                     // the stage's group
-        int slot = gslot + D;
-        if (slot >= NS) slot -= NS;
+        int slot = gslot + D % NS;                                 // (gslot + D) mod NS, gslot < NS
         if (slot >= NS) slot -= NS;
         const uint32_t m0 = lds_e + (uint32_t)slot * Q8_STAGE + (uint32_t)(wave * RPW) * Q2_SB;
         const uint32_t soff = (uint32_t)lane * 16;                 // lanes past the side data idle
@@ -503,7 +502,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         Step a0[Q8_EB], a1[Q8_EB], a2[Q8_EB];
         static_for<SPG>([&](auto jc) __attribute__((always_inline)) {
             constexpr int j = decltype(jc)::value;
-            int sl = gslot + j, sln = gslot + j + 1;               // ring slots of stages t, t + 1
+            int sl = gslot + j % NS, sln = gslot + (j + 1) % NS;  // ring slots of stages t, t + 1
             if (sl >= NS) sl -= NS;
             if (sln >= NS) sln -= NS;
             const uint8_t* sb = sm.e + sl * Q8_STAGE;
@@ -560,7 +559,7 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     auto next_group = [&]() __attribute__((always_inline)) {
         gbase += grp_bytes;
         fbase += Q8_GR;
-        gslot += SPG;
+        gslot += SPG % NS;                                         // correct also if a group spans more stages than the ring
         if (gslot >= NS) gslot -= NS;
     };
     for (int gi = 0; gi < ng; gi += 2) {
