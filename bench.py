@@ -39,9 +39,9 @@ TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_am
                    "paper_2502_06798_amd/csrc/qs_e4m3.hip", "paper_2502_06798_amd/csrc/qs8_kernel.h",
                    "paper_2502_06798_amd/csrc/qs8_f16.hip", "paper_2502_06798_amd/csrc/qs8_bf16.hip",
                    "paper_2502_06798_amd/csrc/qs8_e4m3.hip", "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "a42a158f1d6f0a37"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160773548, "b1024_n1m_d768_bf16": 1571184592,
-                 "b4096_n4m_d512_f16": 4369373394, "b16384_n10m_d768_e4m3": 129667118298}
+TRAFFIC_SHA256 = "c0d04360902003ea"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160792891, "b1024_n1m_d768_bf16": 1577024850,
+                 "b4096_n4m_d512_f16": 15325929304, "b16384_n10m_d768_e4m3": 198683897357}
 
 
 def log(*a):
