@@ -111,6 +111,51 @@ void apc_destroy_cache(apc_cache* c);
 apc_status apc_row_factors(apc_dtype dt, int64_t n, int32_t d, const void* rows, float* out,
                            void* stream);
 
+/*
+ * Storage of float32 embeddings in a cache type (the step before
+ * apc_build_cache or apc_match_batch for a caller that holds float32
+ * vectors; the paper keeps prompt embeddings in its cache and fixes no
+ * storage type, so this recipe is the library's):
+ *   APC_F16, APC_BF16  each element rounded to nearest-even (overflow gives
+ *                      +-Inf; NaN gives a quiet NaN of the same sign);
+ *   APC_E4M3           per row the scale s = amax / 448 (amax = the largest
+ *                      |x| of the row, float32 division; s = 1 when it is not
+ *                      > 0, which includes a row holding NaN), then each
+ *                      element's e4m3fn code of clamp(x / s, -448, 448)
+ *                      rounded to nearest-even (NaN gives 0x7f with its sign).
+ * x          n x d float32 rows (device, 16-byte aligned, caller-owned).
+ * out        n x d elements of dt (device, 16-byte aligned; d * element
+ *            size a multiple of 16 bytes).
+ * row_scale  n float32 (device; APC_E4M3 only, else NULL): the scales s.
+ * dt = APC_F32 is APC_E_DTYPE; a missing, extra or misaligned pointer or a
+ * row size that is not a multiple of 16 bytes is APC_E_ARG, returned before
+ * anything is enqueued.  n = 0 is a no-op.  Asynchronous on stream.
+ */
+apc_status apc_quantize_rows(apc_dtype dt, int64_t n, int32_t d, const float* x, void* out, float* row_scale,
+                             void* stream);
+
+/*
+ * Checks n rows of type dt as apc_build_cache checks cache rows (the
+ * per-row preparation of the Query Dispatcher's retrieval: a row whose
+ * cosine is undefined cannot be matched), for example a batch of queries
+ * before apc_match_batch.  Bits of a row's flag: 1 = a non-finite element,
+ * or a float32 sum of squares that is not finite (elements whose squares
+ * overflow); 2 = zero norm (the float32 sum of squares is 0: every element
+ * is at most 2^-75 in magnitude); 4 = (APC_E4M3) the row scale is not
+ * finite and > 0.
+ * rows       n x d elements of dt (device, 16-byte aligned; d * element
+ *            size a multiple of 16 bytes).
+ * row_scale  n float32 (device; APC_E4M3 only, else NULL).
+ * bad        n uint8 flags (device, may be NULL).
+ * n_bad      (host) number of rows with a flag; first_bad (host, may be
+ *            NULL) the lowest such row, or -1.
+ * Argument errors (as apc_quantize_rows; n_bad NULL) return APC_E_ARG or
+ * APC_E_DTYPE before anything is enqueued.  Allocates a few bytes of device
+ * memory per call and waits for the stream.  n = 0 is a no-op.
+ */
+apc_status apc_validate_rows(apc_dtype dt, int64_t n, int32_t d, const void* rows, const float* row_scale,
+                             uint8_t* bad, int64_t* n_bad /* host */, int64_t* first_bad /* host */, void* stream);
+
 /* Copies the handle's n entry factors to out (n float32, device). */
 apc_status apc_cache_row_factors(const apc_cache* c, float* out, void* stream);
 

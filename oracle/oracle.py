@@ -436,3 +436,114 @@ def merge_shards(scores, idx, offsets, k: int):
         for j, (sc, e) in enumerate(cand[:k]):
             out_s[q, j], out_i[q, j] = sc, e
     return out_s, out_i
+
+
+# ---- Storage of float32 rows in a cache type, and row checks ----------------
+# The paper keeps prompt embeddings in its cache and fixes no storage type;
+# the library's recipe is: binary16 and bfloat16 by rounding each element to
+# the nearest representable value (ties to the even one, overflow to +-Inf),
+# e4m3fn with one float32 scale per row s = amax / 448 (s = 1 when it is not
+# > 0, a row holding NaN included) and the codes of clamp(x / s, -448, 448),
+# rounded to the nearest code value with ties to the even code.  Written out
+# from the formats' value sets, not from bit tricks.
+
+def e4m3_values() -> np.ndarray:
+    """Value of each of the 256 e4m3fn codes (NaN for 0x7f and 0xff): sign,
+    4 exponent bits (bias 7), 3 mantissa bits; exponent 0 is subnormal."""
+    v = np.empty(256, dtype=np.float64)
+    for c in range(256):
+        e, m = (c >> 3) & 15, c & 7
+        if e == 15 and m == 7:
+            v[c] = np.nan
+            continue
+        mag = (m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+        v[c] = -mag if c & 0x80 else mag
+    return v
+
+
+def _sign_bits(y32: np.ndarray) -> np.ndarray:
+    return (y32.view(np.uint32) >> 31).astype(np.uint8)
+
+
+def round_e4m3(y: np.ndarray) -> np.ndarray:
+    """e4m3fn codes of float32 values |y| <= 448 (or NaN): the nearest code
+    value, ties to the even code (codes 0..126 grow with their value, and the
+    even one of two neighbours has the even mantissa).  NaN gives 0x7f with
+    its sign."""
+    y32 = np.asarray(y, dtype=np.float32)
+    mags = e4m3_values()[:127]                                    # codes 0 .. 126, ascending
+    a = np.abs(y32.astype(np.float64))
+    if np.any(a[~np.isnan(a)] > 448.0):
+        raise ValueError("round_e4m3: |y| > 448")
+    hi = np.clip(np.searchsorted(mags, np.nan_to_num(a, nan=0.0), side="left"), 0, 126)
+    lo = np.clip(hi - 1, 0, 126)
+    dlo, dhi = a - mags[lo], mags[hi] - a
+    code = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi))).astype(np.uint8)
+    code = np.where(np.isnan(a), 0x7f, code).astype(np.uint8)
+    return (code | (_sign_bits(y32) << 7)).astype(np.uint8)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """bfloat16 codes (uint16) of float32 values: of the two bfloat16 values
+    around x (its float32 bits with the low 16 cleared, and the next one up in
+    magnitude; past the largest finite one stands 2^128, i.e. Inf), the
+    nearer, ties to the one with the even code.  NaN gives a quiet NaN of the
+    same sign."""
+    x32 = np.asarray(x, dtype=np.float32)
+    u = x32.view(np.uint32)
+    t = u & np.uint32(0xFFFF0000)                                 # toward zero
+    up = t + np.uint32(0x10000)                                   # away from zero
+    def mag(bits):
+        e = (bits >> 23) & 0xFF
+        frac = (bits & 0x7FFFFF).astype(np.float64)
+        m = np.where(e == 0, frac / 2.0 ** 23 * 2.0 ** -126, (1.0 + frac / 2.0 ** 23) * 2.0 ** (e.astype(np.float64) - 127))
+        return np.where(e == 255, 2.0 ** 128, m)                  # the exponent of Inf, as its value would be
+    a = np.abs(x32.astype(np.float64))
+    dt, du = a - mag(t & 0x7FFFFFFF), mag(up & 0x7FFFFFFF) - a
+    pick_up = np.where(du < dt, True, np.where(dt < du, False, ((t >> 16) & 1) == 1))
+    out = np.where(pick_up, up >> 16, t >> 16).astype(np.uint32)
+    out = np.where(np.isinf(x32), u >> 16, out)                   # +-Inf stays
+    out = np.where(np.isnan(x32), (u >> 16) | 0x40, out)
+    return out.astype(np.uint16)
+
+
+def quantize_rows(dtype: str, x: np.ndarray):
+    """(stored rows, float32 row scales or None) of float32 rows x."""
+    x32 = np.ascontiguousarray(x, dtype=np.float32)
+    if dtype == "f16":
+        with np.errstate(over="ignore"):
+            return x32.astype(np.float16), None
+    if dtype == "bf16":
+        return round_bf16(x32), None
+    if dtype != "e4m3":
+        raise ValueError(f"quantize_rows: no such target {dtype}")
+    with np.errstate(invalid="ignore", divide="ignore", over="ignore"):
+        amax = np.abs(x32).max(axis=1) if x32.shape[1] else np.zeros(x32.shape[0], np.float32)
+        s = np.where(np.isnan(x32).any(axis=1), np.float32(np.nan), amax / np.float32(448.0)).astype(np.float32)
+        s = np.where(s > 0, s, np.float32(1.0)).astype(np.float32)
+        y = (x32 / s[:, None]).astype(np.float32)
+        y = np.where(np.isnan(y), y, np.clip(y, np.float32(-448.0), np.float32(448.0))).astype(np.float32)
+    return round_e4m3(y), s
+
+
+NONFINITE, ZERO_NORM, BAD_SCALE = 1, 2, 4
+
+
+def validate_rows(dtype: str, rows: np.ndarray, scale=None) -> np.ndarray:
+    """Per-row flags: NONFINITE if an element is not finite or the sum of
+    squares reaches 2^128 (it cannot be held in float32); else ZERO_NORM if
+    every element is at most 2^-75 in magnitude (each square rounds to zero
+    in float32); BAD_SCALE (e4m3) if the row's scale is not finite and > 0.
+    For e4m3 the elements are the codes' values (the scale cancels in the
+    cosine).  Near the 2^128 boundary a float32 sum may round either way;
+    this reads the exact sum."""
+    n = np.shape(rows)[0]
+    v = decode(dtype, rows, np.ones(n, np.float32) if dtype == "e4m3" else None)
+    with np.errstate(over="ignore", invalid="ignore"):
+        nonfinite = ~np.isfinite(v).all(axis=1) | ~((v * v).sum(axis=1) < 2.0 ** 128)
+    zero = ~nonfinite & (np.abs(np.nan_to_num(v)) <= 2.0 ** -75).all(axis=1)
+    flags = np.where(nonfinite, NONFINITE, 0) | np.where(zero, ZERO_NORM, 0)
+    if dtype == "e4m3":
+        s = np.asarray(scale, dtype=np.float32)
+        flags |= np.where(np.isfinite(s) & (s > 0), 0, BAD_SCALE)
+    return flags.astype(np.uint8)

@@ -13,8 +13,9 @@ from .binding import (APC_BF16, APC_E4M3, APC_F16, APC_F32, APC_MAX_INST, APC_MA
                       apc_cache_row_factors, apc_destroy_cache, apc_gather_latents,
                       apc_gather_latents_at_level,
                       apc_last_error, apc_level_histogram, apc_match_batch, apc_match_batch_static, apc_match_workspace,
-                      apc_merge_shards, apc_resident_best, apc_route_plan,
-                      apc_row_factors, apc_set_kernel_events, apc_status_str, load, workspace_tensor)
+                      apc_merge_shards, apc_quantize_rows, apc_resident_best, apc_route_plan,
+                      apc_row_factors, apc_set_kernel_events, apc_status_str, apc_validate_rows, load,
+                      workspace_tensor)
 from .pipeline import MatchStep
 
 __all__ = ["APC_BF16", "APC_E4M3", "APC_F16", "APC_F32", "APC_MAX_INST", "APC_MAX_K",
@@ -23,7 +24,8 @@ __all__ = ["APC_BF16", "APC_E4M3", "APC_F16", "APC_F32", "APC_MAX_INST", "APC_MA
            "apc_assign_routed", "apc_build_cache",
            "apc_cache_row_factors", "apc_destroy_cache", "apc_gather_latents",
            "apc_gather_latents_at_level", "apc_last_error",
-           "apc_level_histogram", "apc_match_batch", "apc_match_batch_static", "apc_match_workspace", "apc_merge_shards", "apc_resident_best",
+           "apc_level_histogram", "apc_match_batch", "apc_match_batch_static", "apc_match_workspace", "apc_merge_shards",
+           "apc_quantize_rows", "apc_resident_best",
            "apc_route_plan", "apc_row_factors", "apc_set_kernel_events",
-           "apc_status_str", "load",
+           "apc_status_str", "apc_validate_rows", "load",
            "workspace_tensor"]

@@ -56,6 +56,10 @@ def load() -> ctypes.CDLL:
     L.apc_destroy_cache.restype = None
     L.apc_row_factors.argtypes = [ctypes.c_int, i64, i32, vp, vp, vp]
     L.apc_row_factors.restype = st
+    L.apc_quantize_rows.argtypes = [ctypes.c_int, i64, i32, vp, vp, vp, vp]
+    L.apc_quantize_rows.restype = st
+    L.apc_validate_rows.argtypes = [ctypes.c_int, i64, i32, vp, vp, vp, ctypes.POINTER(i64), ctypes.POINTER(i64), vp]
+    L.apc_validate_rows.restype = st
     L.apc_cache_row_factors.argtypes = [vp, vp, vp]
     L.apc_cache_row_factors.restype = st
     L.apc_match_workspace.argtypes = [vp, i32, i32, ctypes.POINTER(sz)]
@@ -185,6 +189,21 @@ def apc_destroy_cache(c: Cache):
 def apc_row_factors(rows: torch.Tensor, out: torch.Tensor, stream=None):
     n, d = rows.shape
     _check(load().apc_row_factors(DTYPE_OF[rows.dtype], n, d, _ptr(rows), _ptr(out), _stream(stream)))
+
+
+def apc_quantize_rows(x: torch.Tensor, out: torch.Tensor, row_scale=None, stream=None):
+    """float32 rows x into out (f16, bf16 or e4m3fn; row_scale for e4m3fn)."""
+    n, d = x.shape
+    _check(load().apc_quantize_rows(DTYPE_OF[out.dtype], n, d, _ptr(x), _ptr(out), _ptr(row_scale), _stream(stream)))
+
+
+def apc_validate_rows(rows: torch.Tensor, row_scale=None, bad=None, stream=None):
+    """(bad-row count, lowest bad row or -1); per-row flags into bad (uint8) if given."""
+    n, d = rows.shape
+    nb, fb = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().apc_validate_rows(DTYPE_OF[rows.dtype], n, d, _ptr(rows), _ptr(row_scale), _ptr(bad),
+                                    ctypes.byref(nb), ctypes.byref(fb), _stream(stream)))
+    return nb.value, fb.value
 
 
 def apc_cache_row_factors(c: Cache, out: torch.Tensor, stream=None):

@@ -136,6 +136,53 @@ apc_status apc_row_factors(apc_dtype dt, int64_t n, int32_t d, const void* rows,
     return ok();
 }
 
+apc_status apc_quantize_rows(apc_dtype dt, int64_t n, int32_t d, const float* x, void* out, float* row_scale,
+                             void* stream)
+{
+    if (valid_dtype(dt) && dt == APC_F32)
+        return fail(APC_E_DTYPE, "apc_quantize_rows: the target must be f16, bf16 or e4m3");
+    apc_status st = check_rows(dt, n, d, out, "apc_quantize_rows");
+    if (st != APC_OK) return st;
+    if (n > 0 && (!x || !aligned16(x)))
+        return fail(APC_E_ARG, "apc_quantize_rows: x must be a non-NULL 16-byte aligned device pointer");
+    if (n > 0 && (dt == APC_E4M3) != (row_scale != nullptr))
+        return fail(APC_E_ARG, "apc_quantize_rows: row_scale is required for e4m3 and only for e4m3");
+    if (n == 0) return ok();
+    hipError_t e = apc::launch_quantize_rows(dt, n, d, x, out, row_scale, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "quantize launch");
+    return ok();
+}
+
+apc_status apc_validate_rows(apc_dtype dt, int64_t n, int32_t d, const void* rows, const float* row_scale,
+                             uint8_t* bad, int64_t* n_bad, int64_t* first_bad, void* stream)
+{
+    if (!n_bad) return fail(APC_E_ARG, "apc_validate_rows: n_bad is NULL");
+    *n_bad = 0;
+    if (first_bad) *first_bad = -1;
+    apc_status st = check_rows(dt, n, d, rows, "apc_validate_rows");
+    if (st != APC_OK) return st;
+    if (n > 0 && (dt == APC_E4M3) != (row_scale != nullptr))
+        return fail(APC_E_ARG, "apc_validate_rows: row_scale is required for e4m3 and only for e4m3");
+    if (n == 0) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    apc::BuildStatus* dst = nullptr;
+    apc::BuildStatus hst{};
+    hst.first_bad = ~0ull;
+    hipError_t e = hipMalloc(&dst, sizeof(apc::BuildStatus));
+    if (e != hipSuccess) return fail(APC_E_NOMEM, "apc_validate_rows: hipMalloc: %s", hipGetErrorString(e));
+    if ((e = hipMemcpyAsync(dst, &hst, sizeof hst, hipMemcpyHostToDevice, s)) != hipSuccess ||
+        (e = apc::launch_row_factors(dt, n, d, rows, row_scale, nullptr, 0, nullptr, dst, s, bad)) != hipSuccess ||
+        (e = hipMemcpyAsync(&hst, dst, sizeof hst, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess) {
+        (void)hipFree(dst);
+        return hip_fail(e, "apc_validate_rows");
+    }
+    (void)hipFree(dst);
+    *n_bad = (int64_t)hst.n_bad;
+    if (first_bad) *first_bad = hst.n_bad ? (int64_t)hst.first_bad : -1;
+    return ok();
+}
+
 apc_status apc_build_cache(apc_dtype dt, int64_t n, int32_t d, const void* emb, const float* row_scale,
                            const void* latents, int64_t n_slots, int64_t latent_bytes,
                            const int32_t* slot_of_entry, void* stream, apc_cache** out)

@@ -26,13 +26,20 @@ struct BuildStatus {
     uint32_t flags;
     uint32_t pad;
     unsigned long long first_bad;   // lowest bad row (or entry) index
+    unsigned long long n_bad;       // bad rows (or entries)
 };
 
-// f[r] = 1/|row r| (NaN for bad rows); when st != nullptr also records bad
-// rows, non-positive or non-finite scales and out-of-range slots.
+// f[r] = 1/|row r| (NaN for bad rows; f may be null); when st != nullptr
+// also records bad rows, non-positive or non-finite scales and out-of-range
+// slots; when rowflags != nullptr writes each row's ST_ bits there.
 hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, const float* scale,
                               const int32_t* slot_of_entry, int64_t n_slots, float* f,
-                              BuildStatus* st, hipStream_t s);
+                              BuildStatus* st, hipStream_t s, uint8_t* rowflags = nullptr);
+
+// float32 rows to a storage type (f16/bf16 rounded to nearest-even; e4m3fn
+// codes with a per-row scale amax / 448 and a clamp to +-448)
+hipError_t launch_quantize_rows(int dt, int64_t n, int32_t d, const float* x, void* out, float* scale,
+                                hipStream_t s);
 
 // factor layout of a cache: n rounded up to a multiple of 256 factors, zeros past n
 __host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void k_row_factors(const uint8_t* __restrict__
                                                       int64_t row_bytes, const float* __restrict__ scale,
                                                       const int32_t* __restrict__ slot_of_entry,
                                                       int64_t n_slots, float* __restrict__ f,
-                                                      BuildStatus* __restrict__ st)
+                                                      BuildStatus* __restrict__ st, uint8_t* __restrict__ rowflags)
 {
     const int lane = threadIdx.x & 63;
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -86,16 +86,16 @@ __global__ __launch_bounds__(256) void k_row_factors(const uint8_t* __restrict__
         float s = scale[r];
         if (!(__builtin_isfinite(s) && s > 0.f)) flags |= ST_SCALE;
     }
-    f[r] = flags ? __int_as_float(0x7fc00000) : 1.0f / __builtin_sqrtf(ss);
-    if (st) {
-        if (slot_of_entry) {
-            int32_t v = slot_of_entry[r];
-            if (v < -1 || (int64_t)v >= n_slots) flags |= ST_SLOT;
-        }
-        if (flags) {
-            atomicOr(&st->flags, flags);
-            atomicMin(&st->first_bad, (unsigned long long)r);
-        }
+    if (f) f[r] = flags ? __int_as_float(0x7fc00000) : 1.0f / __builtin_sqrtf(ss);
+    if (slot_of_entry) {
+        int32_t v = slot_of_entry[r];
+        if (v < -1 || (int64_t)v >= n_slots) flags |= ST_SLOT;
+    }
+    if (rowflags) rowflags[r] = (uint8_t)flags;
+    if (st && flags) {
+        atomicOr(&st->flags, flags);
+        atomicMin(&st->first_bad, (unsigned long long)r);
+        atomicAdd(&st->n_bad, 1ull);
     }
 }
 
@@ -103,17 +103,17 @@ __global__ __launch_bounds__(256) void k_row_factors(const uint8_t* __restrict__
 
 hipError_t launch_row_factors(int dt, int64_t n, int32_t d, const void* rows, const float* scale,
                               const int32_t* slot_of_entry, int64_t n_slots, float* f,
-                              BuildStatus* st, hipStream_t s)
+                              BuildStatus* st, hipStream_t s, uint8_t* rowflags)
 {
     if (n <= 0) return hipSuccess;
     const int64_t row_bytes = (int64_t)d * elem_bytes(dt);
     const dim3 grid((unsigned)((n + 3) / 4)), block(256);
     const uint8_t* r = static_cast<const uint8_t*>(rows);
     switch (dt) {
-    case APC_F32: k_row_factors<APC_F32><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st); break;
-    case APC_F16: k_row_factors<APC_F16><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st); break;
-    case APC_BF16: k_row_factors<APC_BF16><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st); break;
-    default: k_row_factors<APC_E4M3><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st); break;
+    case APC_F32: k_row_factors<APC_F32><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st, rowflags); break;
+    case APC_F16: k_row_factors<APC_F16><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st, rowflags); break;
+    case APC_BF16: k_row_factors<APC_BF16><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st, rowflags); break;
+    default: k_row_factors<APC_E4M3><<<grid, block, 0, s>>>(r, n, row_bytes, scale, slot_of_entry, n_slots, f, st, rowflags); break;
     }
     return hipGetLastError();
 }

@@ -137,3 +137,24 @@ def test_load_aware_argument_errors(lib):
     bad = np.array([0, 3], np.int32)
     assert lib.apc_assign_load_aware(FAKE, 1, 4, 2, p(th), p(Kh), 2, p(bad), p(ic), None, p(rnd), 5, 1,
                                      ctypes.byref(routing), FAKE, FAKE, FAKE, FAKE, FAKE, None) == E_TABLE
+
+
+def test_quantize_and_validate_argument_checks(lib):
+    q = lambda dt, n=4, d=16, x=FAKE, out=FAKE, sc=None: lib.apc_quantize_rows(dt, n, d, x, out, sc, None)
+    assert q(0) == E_DTYPE                                  # float32 is not a storage target
+    assert q(7) == E_DTYPE
+    assert q(3) == E_ARG                                    # e4m3 without scales
+    assert q(1, sc=FAKE) == E_ARG                           # scales for f16
+    assert q(1, x=None) == E_ARG
+    assert q(1, x=ctypes.c_void_p(0x100004)) == E_ARG       # x misaligned
+    assert q(1, d=12) == E_ARG                              # 24-byte rows
+    assert q(1, n=0) == 0                                   # nothing to do
+    nb, fb = ctypes.c_int64(7), ctypes.c_int64(7)
+    v = lambda dt, n=4, d=16, rows=FAKE, sc=None, nbp=ctypes.byref(nb): lib.apc_validate_rows(
+        dt, n, d, rows, sc, None, nbp, ctypes.byref(fb), None)
+    assert v(1, nbp=None) == E_ARG
+    assert v(9) == E_DTYPE
+    assert v(3) == E_ARG                                    # e4m3 without scales
+    assert v(0, sc=FAKE) == E_ARG
+    assert v(1, rows=ctypes.c_void_p(0x100002)) == E_ARG
+    assert v(1, n=0) == 0 and nb.value == 0 and fb.value == -1
