@@ -171,6 +171,9 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
         for (int s = 0; s < C::QST; ++s) qv[s] = *reinterpret_cast<const Step*>(qblk + (int64_t)s * 64 * sizeof(Step));
     }
     const float fq = fq_ws[q0w + r32];
+    // 1 / fq for the exact test's threshold (1024-byte rows: no register to
+    // spare, the threshold divides)
+    const float rfq = RB == 1024 ? 0.f : 1.0f / fq;
     // wait for these loads here: inside the loop the compiler's own waits
     // would also drain the ring's loads, which it does not see
 #pragma unroll
@@ -272,35 +275,72 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
     // (every access of a list goes through uint64_t, so that the compiler
     // keeps a lane's stores and its partner's later loads in order)
     uint64_t* const lst = reinterpret_cast<uint64_t*>(sm.lst + (wave * 32 + r32) * C::LSTR);
+    // slots from k on (this lane's) hold the largest key, for the rescans
+#pragma unroll
+    for (int i = 0; i < KR / 2; ++i) {
+        const int sl = 2 * h + 4 * (i >> 1) + (i & 1);
+        if (sl >= k) lst[sl] = ~0ull;
+    }
     int cnt = 0;                 // keys in the list
     uint64_t wkey = 0;           // its smallest key (valid once cnt == k)
     int wslot = 0;               // and that key's slot
     float own = neg_inf();       // the list's k-th best score (-inf while cnt < k)
     uint64_t hkey = ~0ull;       // the smallest key of this lane's slots
     int hslot = 0;               // and its slot
-    // the smallest of this lane's keys and its slot (four reads, eight keys,
-    // at a time)
+    // the smallest of this lane's keys and its slot (slots from k on hold the
+    // largest key, so they are never the smallest of a full list): its KR / 2
+    // slots read eight at a time, each eight through a tree of comparisons;
+    // for 1024-byte rows, whose registers are full, in a loop over the first k
     auto rescan = [&]() __attribute__((always_inline)) {
-        uint64_t best = ~0ull;
-        int bs = 0;
+        if constexpr (RB == 1024) {
+            uint64_t best = ~0ull;
+            int bs = 0;
 #pragma unroll 1
-        for (int c0 = 2 * h; c0 < k; c0 += 16) {                  // slots c0 + 4 i, + 1: this half's
-            uint64_t v[8];
+            for (int c0 = 2 * h; c0 < k; c0 += 16) {               // slots c0 + 4 i, + 1: this half's
+                uint64_t v[8];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                v[2 * i] = lst[c0 + 4 * i];
-                v[2 * i + 1] = lst[c0 + 4 * i + 1];
-            }
+                for (int i = 0; i < 4; ++i) {
+                    v[2 * i] = lst[c0 + 4 * i];
+                    v[2 * i + 1] = lst[c0 + 4 * i + 1];
+                }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint64_t k0 = v[2 * i], k1 = v[2 * i + 1];
-                const int p0 = c0 + 4 * i;
-                if (p0 < k && k0 < best) { best = k0; bs = p0; }
-                if (p0 + 1 < k && k1 < best) { best = k1; bs = p0 + 1; }
+                for (int i = 0; i < 4; ++i) {
+                    const uint64_t k0 = v[2 * i], k1 = v[2 * i + 1];
+                    const int p0 = c0 + 4 * i;
+                    if (p0 < k && k0 < best) { best = k0; bs = p0; }
+                    if (p0 + 1 < k && k1 < best) { best = k1; bs = p0 + 1; }
+                }
             }
+            hkey = best;
+            hslot = bs;
+        } else {
+            constexpr int HS = KR / 2, CH = HS < 8 ? HS : 8;
+            uint64_t best = ~0ull;
+            int bs = 0;
+#pragma unroll 1
+            for (int c0 = 0; c0 < HS; c0 += CH) {
+                uint64_t v[CH];
+                int vs[CH];
+#pragma unroll
+                for (int i = 0; i < CH; ++i) {
+                    vs[i] = 2 * h + 4 * ((c0 + i) >> 1) + ((c0 + i) & 1);   // this half's slots
+                    v[i] = lst[vs[i]];
+                }
+#pragma unroll
+                for (int w = 1; w < CH; w *= 2)
+#pragma unroll
+                    for (int i = 0; i + w < CH; i += 2 * w) {
+                        const bool tk = v[i + w] < v[i];
+                        v[i] = tk ? v[i + w] : v[i];
+                        vs[i] = tk ? vs[i + w] : vs[i];
+                    }
+                const bool tk = v[0] < best;
+                best = tk ? v[0] : best;
+                bs = tk ? vs[0] : bs;
+            }
+            hkey = best;
+            hslot = bs;
         }
-        hkey = best;
-        hslot = bs;
     };
     // the list's smallest key and slot from both lanes' (all lanes take part)
     auto combine = [&]() __attribute__((always_inline)) {
@@ -348,10 +388,12 @@ __global__ __launch_bounds__(Q8_NT) void k_qs8(
             } else {
                 // the pairs whose score can reach F: y fq >= F implies y >= Fy,
                 // Fy = F / fq moved away from zero by far more than the rounding
-                // of either side.  This admits a few more pairs than the exact
-                // test; each is then kept only if its exact key beats the
-                // list's smallest, so the list is unchanged by the extras.
-                const float fy = F / fq;
+                // of either side (F times the rounded 1 / fq is within 2^-23 of
+                // F / fq, relative; the margin is 2^-18).  This admits a few
+                // more pairs than the exact test; each is then kept only if its
+                // exact key beats the list's smallest, so the list is unchanged
+                // by the extras.
+                const float fy = RB == 1024 ? F / fq : F * rfq;
                 const float Fy = fy > 0.f ? fy * (1.f - 0x1p-18f) : fy * (1.f + 0x1p-18f);
 #pragma unroll
                 for (int j = 31; j >= 0; --j) mask = q2_shift_in(mask, prv[j >> 4][j & 15] >= Fy);
