@@ -51,7 +51,7 @@ constexpr int Q8_LPW = Q8_STAGE / 1024 / Q8_NW; // row loads per wavefront per s
 constexpr int Q8_OPS = Q8_LPW + 1;              // vector-memory operations per wavefront per stage
 constexpr int Q8_FR = 8;                        // ring of per-group entry factors
 constexpr int Q8_KMAX = 32;
-constexpr int Q8_QM = 128;                      // groups between refreshes of the quantile bound
+constexpr int Q8_QM = 256;                      // groups between refreshes of the quantile bound
 constexpr int Q8_QSPLITS = 16;                  // most splits it is shared over
 
 template <int DT, int RB, int KR>
