@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libapc.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "qs8_f16.hip", "qs8_bf16.hip", "qs8_e4m3.hip", "assign.hip", "gather.hip", "resident.hip", "shards.hip", "quantize.hip"]
+SOURCES = ["apc.cpp", "rowfactor.hip", "simtopk.hip", "stream.hip", "qs.hip", "qs_f16.hip", "qs_bf16.hip", "qs_e4m3.hip", "qs8_f16.hip", "qs8_bf16.hip", "qs8_e4m3.hip", "assign.hip", "gather.hip", "resident.hip", "shards.hip", "quantize.hip", "f32small.hip"]
 
 # Kernels in these sources load into LDS with asm and wait for those loads by
 # counting vector-memory operations themselves; a register spill would add

@@ -45,7 +45,7 @@ hipError_t launch_quantize_rows(int dt, int64_t n, int32_t d, const float* x, vo
 __host__ __device__ inline int64_t factor_pad(int64_t n) { return (n + 255) / 256 * 256; }
 
 // ---- similarity + top-k ----------------------------------------------------
-enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QS = 4, KERNEL_QS8 = 5 };
+enum { KERNEL_TILED = 0, KERNEL_STREAM_64 = 1, KERNEL_STREAM_32 = 2, KERNEL_QS = 4, KERNEL_QS8 = 5, KERNEL_F32S = 6 };
 struct MatchPlan {
     int kernel;        // kernel variant id
     int bq;            // queries per workgroup tile
@@ -92,6 +92,15 @@ int qs8_group_rows();
 hipError_t launch_qs8(const MatchPlan& p, int dt, int64_t n, int32_t d, const void* emb, const float* fe,
                       const void* q, const float* fq, int* gthr, int* g2, int32_t b, int32_t k, float* ps, int* pi,
                       hipStream_t s);
+
+// float32 caches of at most 512 blocks of 32 rows, d a multiple of 64, k <= 32,
+// b <= 256: one workgroup per 32-row block and 16-query tile, four wavefronts
+// over d (f32small.hip); the query factors come first from launch_row_factors
+bool f32s_fits(int dt, int64_t n, int32_t d, int32_t b, int32_t k);
+int f32s_queries();
+int f32s_rows();
+hipError_t launch_f32s(const MatchPlan& p, int64_t n, int32_t d, const void* emb, const float* fe, const void* q,
+                       const float* fq, int32_t b, int32_t k, float* ps, int* pi, hipStream_t s);
 
 // ---- assignment ------------------------------------------------------------
 struct AssignTable {

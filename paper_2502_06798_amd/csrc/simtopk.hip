@@ -510,6 +510,12 @@ MatchPlan plan_match(int dt, int64_t n, int32_t d, int32_t b, int32_t k)
         if (splits > ngr) splits = ngr;
         if (splits < 1) splits = 1;
         p.splits = (int)splits;
+    } else if (f32s_fits(dt, n, d, b, k)) {
+        // small float32 caches: a workgroup per 32-row block, d over its wavefronts
+        p.kernel = KERNEL_F32S;
+        p.bq = f32s_queries();
+        p.qtiles = (b + p.bq - 1) / p.bq;
+        p.splits = (int)((n + f32s_rows() - 1) / f32s_rows());
     } else if (b <= 256 && rb <= 3072 && rb % group == 0) {
         // small batch: query tile resident in LDS, entries streamed from HBM
         const bool wide = k <= 16 && rb <= 1536 && dt != APC_E4M3;
@@ -572,6 +578,10 @@ hipError_t launch_match(const MatchPlan& p, int dt, int64_t n, int32_t d, const 
         case APC_BF16: e = run_simtopk_k<APC_BF16>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         default: e = run_simtopk_k<APC_E4M3>(p, n, emb, fe, q, fq, b, row_bytes, k, ps, pi, s); break;
         }
+    } else if (p.kernel == KERNEL_F32S) {
+        if ((e = launch_row_factors(dt, b, d, q, q_scale, nullptr, 0, fq, nullptr, s)) != hipSuccess) return e;
+        if (ev_start && (e = hipEventRecord(ev_start, s)) != hipSuccess) return e;
+        e = launch_f32s(p, n, d, emb, fe, q, fq, b, k, ps, pi, s);
     } else if (p.kernel == KERNEL_QS) {
         int* gt = reinterpret_cast<int*>(w + p.off_gt);
         uint8_t* qp = w + p.off_qp;

@@ -90,10 +90,19 @@ CASES = [
     ("e4m3", 64, 3000, 768, 32),
     ("e4m3", 200, 1500, 112, 7),
     ("f16", 300, 129, 64, 64),
-    # streaming kernel: float rows, and 16-bit or e4m3 rows of sizes the
-    # query-stationary kernel is not built for (whole groups of 4 x 128 bytes,
-    # 6 x 128 for e4m3), or k > 32
+    # float32 caches of at most 512 blocks of 32 rows (d a multiple of 64,
+    # k <= 32, b <= 256): a workgroup per block, d over its wavefronts; a
+    # partial last block, one query, the largest cache, k = 32, partial and
+    # many query tiles
     ("f32", 16, 5000, 768, 5),
+    ("f32", 1, 33, 128, 1),
+    ("f32", 17, 16384, 256, 32),
+    ("f32", 256, 2000, 64, 12),
+    ("f32", 40, 70, 1024, 7),
+    # streaming kernel: larger float caches, and 16-bit or e4m3 rows of sizes
+    # the query-stationary kernel is not built for (whole groups of 4 x 128
+    # bytes, 6 x 128 for e4m3), or k > 32
+    ("f32", 16, 20000, 768, 5),
     ("f16", 64, 1000, 1536, 12),
     # query-stationary kernel: 16-bit or e4m3 rows of 512, 768, 1024 or 1536
     # bytes, k <= 32; every shape family (rows, query blocks, 32-row blocks per
