@@ -39,9 +39,9 @@ TRAFFIC_SOURCES = ("paper_2502_06798_amd/csrc/qs_kernel.h", "paper_2502_06798_am
                    "paper_2502_06798_amd/csrc/qs_e4m3.hip", "paper_2502_06798_amd/csrc/qs8_kernel.h",
                    "paper_2502_06798_amd/csrc/qs8_f16.hip", "paper_2502_06798_amd/csrc/qs8_bf16.hip",
                    "paper_2502_06798_amd/csrc/qs8_e4m3.hip", "paper_2502_06798_amd/csrc/simtopk.hip")
-TRAFFIC_SHA256 = "38b5574c16513977"
-TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160789382, "b1024_n1m_d768_bf16": 1575309407,
-                 "b4096_n4m_d512_f16": 13255596318, "b16384_n10m_d768_e4m3": 146944663060}
+TRAFFIC_SHA256 = "0c9372c2c89e4c07"
+TRAFFIC_BYTES = {"b256_n100k_d768_f16": 160786432, "b1024_n1m_d768_bf16": 1573105664,
+                 "b4096_n4m_d512_f16": 13140833280, "b16384_n10m_d768_e4m3": 149277192192}
 
 
 def log(*a):
