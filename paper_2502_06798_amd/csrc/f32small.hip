@@ -4,13 +4,12 @@
 // A small float32 cache gives each CU only a block or two of 32 rows, and one
 // wavefront working through all of d in one accumulation chain is latency
 // bound.  Here a workgroup takes one 32-row block against a tile of 16
-// queries and its wavefronts (eight when d is a multiple of 128, else four)
-// take equal parts of d, with 16x16x4
-// float32 MFMAs (two row tiles of 16); the partial sums meet in LDS.  A lane
-// of wavefront w of NW supplies, at step (t, j), row i = lane % 16 and column
-// w d/NW + 16 t + 4 (lane / 16) + j of both operands, so the two operands see
-// the same column for every product and each lane reads 16 contiguous bytes
-// of its row per step.  Every query's 32 scores then give the block's
+// queries, and its NW wavefronts (eight when d is a multiple of 128, else
+// four) take equal parts of d with 16x16x4 float32 MFMAs (two row tiles of
+// 16); the partial sums meet in LDS.  A lane of wavefront w supplies, at
+// step (t, j), row i = lane % 16 and column w d/NW + 16 t + 4 (lane / 16) + j
+// of both operands, so the two operands see the same column for every
+// product and each lane reads 16 contiguous bytes of its row per step.  Every query's 32 scores then give the block's
 // partial list (k best, sorted by score desc then entry asc, each pair placed
 // by its rank; rows past the cache are -inf), which k_topk_merge merges over
 // the blocks.
