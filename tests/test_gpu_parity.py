@@ -99,6 +99,8 @@ CASES = [
     ("f32", 17, 16384, 256, 32),
     ("f32", 256, 2000, 64, 12),
     ("f32", 40, 70, 1024, 7),
+    ("f32", 3, 1, 64, 1),              # a one-row cache
+    ("f32", 256, 16384, 64, 32),       # the largest batch, cache and k together
     # streaming kernel: larger float caches, and 16-bit or e4m3 rows of sizes
     # the query-stationary kernel is not built for (whole groups of 4 x 128
     # bytes, 6 x 128 for e4m3), or k > 32
@@ -237,27 +239,36 @@ def test_match_two_waves_per_simd(apc, orc, dtype, b, n, d, k):
     c.close()
 
 
-def test_match_ties_take_lower_index(apc, orc):
-    say("match ties")
-    row = torch.randn(1, 64, device="cuda").half()
-    e = row.repeat(1000, 1).contiguous()
-    q = torch.randn(3, 64, device="cuda").half()
-    c = apc.apc_build_cache(e)
-    k = 20
-    ts = torch.empty((3, k), dtype=torch.float32, device="cuda")
-    ti = torch.empty((3, k), dtype=torch.int32, device="cuda")
-    apc.apc_match_batch(c, q, None, k, ts, ti, apc.workspace_tensor(c, 3, k))
+@pytest.mark.parametrize("dtype,d,b,n,k", [
+    ("f16", 64, 3, 1000, 20),        # tiled / streaming kernels
+    ("f32", 64, 3, 1000, 20),        # small float32 caches, four wavefronts over d
+    ("f32", 768, 17, 5000, 32),      # the same, eight wavefronts
+    ("f16", 768, 5, 3000, 10),       # query-stationary kernel (1536-byte rows)
+    ("e4m3", 768, 300, 2000, 32),    # two wavefronts per SIMD (768-byte rows)
+])
+def test_match_ties_take_lower_index(apc, orc, dtype, d, b, n, k):
+    """Every cache row the same: every score ties, and the top-k is entries
+    0 .. k-1 in order, whatever the kernel."""
+    say(f"match ties {dtype} d={d} b={b} n={n} k={k}")
+    row, rsc = make_rows(1, d, dtype, 77)
+    e = row.repeat(n, 1).contiguous()
+    es = None if rsc is None else rsc.repeat(n).contiguous()
+    q, qs = make_rows(b, d, dtype, 78)
+    c = apc.apc_build_cache(e, es)
+    ts = torch.empty((b, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((b, k), dtype=torch.int32, device="cuda")
+    apc.apc_match_batch(c, q, qs, k, ts, ti, apc.workspace_tensor(c, b, k))
     torch.cuda.synchronize()
-    assert ti.cpu().tolist() == [list(range(k))] * 3
+    assert ti.cpu().tolist() == [list(range(k))] * b
     assert torch.all(ts == ts[:, :1])
     c.close()
 
 
-@pytest.mark.parametrize("d", [32, 256])     # tiled and streaming kernels
-def test_match_invalid_query_rows(apc, d):
-    say(f"match invalid query rows d={d}")
-    e, _ = make_rows(500, d, "f16", 5)
-    q, _ = make_rows(6, d, "f16", 6)
+@pytest.mark.parametrize("dtype,d", [("f16", 32), ("f16", 256), ("f32", 64)])   # tiled, streaming, small float32
+def test_match_invalid_query_rows(apc, dtype, d):
+    say(f"match invalid query rows {dtype} d={d}")
+    e, _ = make_rows(500, d, dtype, 5)
+    q, _ = make_rows(6, d, dtype, 6)
     q[1] = 0
     q[4, 3] = float("inf")
     c = apc.apc_build_cache(e)
